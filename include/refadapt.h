@@ -1,0 +1,212 @@
+/*
+ * refadapt.h - C ABI of the MI355X (gfx950) hot path of RefAdapt-DiT
+ * (arxiv 2609.32415): joint attention over a [reference; target] token
+ * sequence with fresh or cached reference K/V and per-query reference mass,
+ * the consecutive target-Q change, the reuse gate and the cache commit.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensor pointers are DEVICE pointers (memory of the current HIP device);
+ *   descriptors and argument structs are HOST memory read during the call.
+ * - The caller owns every buffer. The library allocates no device memory and
+ *   never synchronises: each call validates its arguments on the host, then
+ *   enqueues kernels on `stream` (a hipStream_t; NULL is the null stream) and
+ *   returns. All calls are stream-ordered and contain no host round-trip.
+ * - Errors: arguments are validated synchronously and a non-zero ra_status is
+ *   returned; nothing is enqueued in that case. refadapt_last_error() gives a
+ *   message for the calling thread's last failing call. Device-side faults
+ *   are asynchronous and surface at the caller's next synchronisation.
+ * - Tensors are [B, H, S, d] with explicit element strides for B, H and S;
+ *   the head dimension d is contiguous (stride 1). bf16 tensors need 16-byte
+ *   aligned base pointers and strides that are multiples of 8 elements;
+ *   fp32 tensors need 16-byte alignment and strides that are multiples of 4.
+ */
+#ifndef REFADAPT_H
+#define REFADAPT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RA_OK = 0,
+  RA_EINVAL = -1,        /* malformed argument (null pointer, bad size or enum) */
+  RA_EUNSUPPORTED = -2,  /* well-formed but not implemented (head_dim, alignment) */
+  RA_EWORKSPACE = -3,    /* workspace missing or too small */
+  RA_ELAUNCH = -4        /* the HIP runtime refused a launch */
+} ra_status;
+
+typedef enum { RA_BF16 = 0, RA_F32 = 1 } ra_dtype;
+
+/* Which query rows attend (paper App. A.4: a cached step drops the two
+ * reference-query score regions). */
+typedef enum {
+  RA_Q_TARGET = 0, /* target queries only: o_tgt (and ref_mass) are written */
+  RA_Q_ALL = 1     /* reference and target queries: o_ref and o_tgt written */
+} ra_qset;
+
+/* Source of the reference segment's K/V. */
+typedef enum {
+  RA_KV_FRESH = 0, /* k_ref / v_ref (this step's reference K/V) */
+  RA_KV_CACHE = 1, /* k_cache / v_cache (the block cache of Sec. 4) */
+  RA_KV_DEVICE = 2 /* chosen on the device from *decision (ra_decision):
+                    *   REUSE      -> target queries only, cached K/V
+                    *   REACTIVATE -> all queries, cached K/V
+                    *   COMPUTE    -> all queries, fresh K/V */
+} ra_kvsrc;
+
+/* Block decisions of Alg. 1 (monotone depth-adaptive reference reuse). */
+typedef enum { RA_REUSE = 0, RA_REACTIVATE = 1, RA_COMPUTE = 2 } ra_decision;
+
+/* Score the gate compares with the block threshold. PRODUCT is the paper's
+ * (Sec. 4 factorized-risk equation, head mean of App. A.2); Q_ONLY and
+ * MASS_ONLY are the single-cue ablations; AND compares mean D and mean M with
+ * a (theta_q, theta_m) pair. */
+typedef enum {
+  RA_GATE_PRODUCT = 0,
+  RA_GATE_Q_ONLY = 1,
+  RA_GATE_MASS_ONLY = 2,
+  RA_GATE_AND = 3
+} ra_gate_mode;
+
+/* A [B, H, S, d] tensor: base pointer and element strides of B, H and S. */
+typedef struct {
+  void* data;
+  int64_t stride_b, stride_h, stride_s;
+} ra_tensor;
+
+typedef struct {
+  int32_t batch, heads, head_dim; /* head_dim in {64, 128} */
+  int32_t n_ref;                  /* reference tokens (>= 0; 0 = plain self-attention) */
+  int32_t n_tgt;                  /* target tokens (>= 1) */
+  int32_t dtype;                  /* ra_dtype of Q/K/V and outputs */
+  float scale;                    /* softmax scale; <= 0 selects 1/sqrt(head_dim) */
+  int32_t qset;                   /* ra_qset (ignored for RA_KV_DEVICE) */
+  int32_t kvsrc;                  /* ra_kvsrc */
+} ra_attn_desc;
+
+typedef struct {
+  ra_tensor q_tgt, k_tgt, v_tgt; /* [B, H, n_tgt, d] target rows */
+  ra_tensor q_ref;               /* [B, H, n_ref, d] reference queries (RA_Q_ALL / DEVICE) */
+  ra_tensor k_ref, v_ref;        /* [B, H, n_ref, d] fresh reference K/V */
+  ra_tensor k_cache, v_cache;    /* [B, H, n_ref, d] cached reference K/V */
+  const int32_t* decision;       /* device word (ra_decision), RA_KV_DEVICE only */
+  ra_tensor o_tgt;               /* out [B, H, n_tgt, d] */
+  ra_tensor o_ref;               /* out [B, H, n_ref, d] (RA_Q_ALL / DEVICE) */
+  float* ref_mass;               /* out [B, H, n_tgt] contiguous fp32, or NULL */
+  float* lse_tgt;                /* out [B, H, n_tgt, 2] = (lse_ref, lse_all), or NULL */
+  float* ref_mass_refq;          /* out [B, H, n_ref] reference-query mass on reference keys, or NULL */
+} ra_attn_args;
+
+/*
+ * refadapt_joint_attn - joint softmax attention over [K_R; K_Y].
+ *
+ * Computes, for every (b, h) and query row q of the selected query set,
+ *   o_q = sum_k softmax_k(scale * q.k) v_k  over keys [K_R; K_Y], values [V_R; V_Y]
+ * (paper Sec. 3.3, fresh/stale-output equations; App. A.4 score regions),
+ * where K_R/V_R are the fresh or cached reference K/V per `kvsrc`, and for
+ * every target query the reference mass
+ *   ref_mass_q = sum_{k in R} A_qk = exp(lse_ref - lse_all)
+ * (Sec. 3.2 directional-exposure equation, before its mean over queries),
+ * obtained from split online-softmax statistics in the same pass; it lies in
+ * [0, 1] by construction and is 0 when n_ref == 0. lse values are natural-log
+ * log-sum-exp of the scaled logits over reference keys / all keys (lse_ref is
+ * -inf when n_ref == 0). Outputs are written in `dtype` (accumulation is fp32,
+ * bf16 MFMA for RA_BF16). Writing ref_mass / lse does not change o (the
+ * attention output is bit-identical with them on or off).
+ *
+ * Under RA_KV_DEVICE the grid covers all queries and reference-query
+ * workgroups exit at once when *decision == RA_REUSE; o_ref is then left
+ * untouched.
+ *
+ * Errors: RA_EINVAL for a null desc/args, sizes out of range, unknown enums,
+ * or a required pointer that is NULL (q/k/v/o_tgt always; k_ref/v_ref when
+ * fresh K/V may be read and n_ref > 0; k_cache/v_cache when cached K/V may be
+ * read and n_ref > 0; q_ref/o_ref when reference queries may attend and
+ * n_ref > 0; decision under RA_KV_DEVICE). RA_EUNSUPPORTED for head_dim not
+ * in {64, 128} or misaligned tensors.
+ */
+ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream);
+
+/*
+ * refadapt_q_change - consecutive relative change of the target queries.
+ *
+ *   d_out[b, h] = ||Q_cur[b,h] - Q_prev[b,h]||_F / (||Q_prev[b,h]||_F + eps)
+ * over the n_tgt x head_dim slice of each (b, h) (paper Sec. 3.1
+ * consecutive-drift equation, applied to post-RoPE target-query heads as in
+ * Sec. 4 "Runtime cues"). Sums are fp32 within a workgroup and fp64 across
+ * workgroups in a fixed order, so the result is bitwise deterministic.
+ *
+ * `workspace` is device memory of at least
+ * refadapt_q_change_workspace_size(...) bytes (scratch for per-chunk partial
+ * sums; contents need no initialisation). d_out is [B, H] contiguous fp32.
+ * Errors: RA_EINVAL (null pointers, sizes), RA_EUNSUPPORTED (alignment),
+ * RA_EWORKSPACE (workspace NULL or smaller than required).
+ */
+size_t refadapt_q_change_workspace_size(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim);
+ra_status refadapt_q_change(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim, int32_t dtype,
+                            ra_tensor q_cur, ra_tensor q_prev, float eps, float* d_out, void* workspace,
+                            size_t ws_bytes, void* stream);
+
+/* Device-resident controller state of one denoising trajectory (Alg. 1). */
+typedef struct {
+  int32_t reactivated; /* an earlier block of the current step reached its threshold */
+  int32_t a_full;      /* step of the last full refresh */
+  int32_t delta_max;   /* bounded-age refresh period; <= 0 disables it */
+  int32_t step;        /* step seen by the last block-0 call */
+} ra_gate_state;
+
+/*
+ * refadapt_gate - one block's reuse decision, on the device.
+ *
+ * With M_h = mean over target queries of mass_prev[b, h, :] (the per-query
+ * reference mass this block's executed attention produced at the previous
+ * step; Sec. 3.2 directional-exposure equation, lagged as in Sec. 4) and
+ * D_h = d_cur[b, h] (refadapt_q_change of this block), the score is
+ * mean over (b, h) of D_h * M_h (Sec. 4 factorized-risk equation; head mean of
+ * App. A.2). Decision (Sec. 4 depth-cutoff equation and the block branch of
+ * Alg. 1): COMPUTE if state->reactivated; else REACTIVATE (and set
+ * state->reactivated) if score >= theta; else REUSE.
+ *
+ * When block == 0 the call first performs the step bookkeeping of Alg. 1:
+ * step 0, or step - a_full >= delta_max (delta_max > 0), is a full refresh
+ * (a_full = step and reactivated = 1, so every block of the step computes);
+ * otherwise reactivated = 0. `theta` is a device array indexed by block:
+ * theta[block] for PRODUCT / Q_ONLY / MASS_ONLY, pairs theta[2*block],
+ * theta[2*block+1] = (theta_q, theta_m) for AND.
+ *
+ * Outputs (device): *decision_out (ra_decision) and score_out[0..2] =
+ * (mean D, mean M, mean D*M). Errors: RA_EINVAL for null pointers, sizes,
+ * block < 0, step < 0 or an unknown mode.
+ */
+ra_status refadapt_gate(int32_t batch, int32_t heads, int32_t n_tgt, int32_t block, int32_t step, int32_t mode,
+                        const float* d_cur, const float* mass_prev, const float* theta, ra_gate_state* state,
+                        int32_t* decision_out, float* score_out, void* stream);
+
+/*
+ * refadapt_cache_commit - refresh a block's reference K/V cache.
+ *
+ * Copies k_ref -> k_cache and v_ref -> v_cache ([B, H, n_ref, d]) when
+ * `decision` is NULL or *decision == RA_COMPUTE, and then writes `step` to
+ * *age when age is non-NULL (Alg. 1: a computing block updates its cached
+ * K/V and sets its materialisation step a_b). Otherwise nothing is written.
+ * Errors: RA_EINVAL (null tensors, sizes), RA_EUNSUPPORTED (alignment).
+ */
+ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int32_t head_dim, int32_t dtype,
+                                ra_tensor k_ref, ra_tensor v_ref, ra_tensor k_cache, ra_tensor v_cache,
+                                const int32_t* decision, int32_t* age, int32_t step, void* stream);
+
+/* Message describing the calling thread's last non-OK status ("" if none). */
+const char* refadapt_last_error(void);
+
+/* Library version string. */
+const char* refadapt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* REFADAPT_H */

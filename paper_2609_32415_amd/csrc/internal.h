@@ -1,0 +1,88 @@
+// Internal interface between the C-ABI layer (api.hip) and the kernels.
+// Nothing here is exported from the shared library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <tuple>
+
+namespace refadapt {
+
+// A [B, H, S, d] view with element strides; d is contiguous.
+struct View {
+  const void* p;
+  int64_t sb, sh, ss;
+};
+
+enum { KV_FRESH = 0, KV_CACHE = 1, KV_DEVICE = 2 };
+enum { DEC_REUSE = 0, DEC_REACTIVATE = 1, DEC_COMPUTE = 2 };
+
+struct AttnParams {
+  View q_tgt, k_tgt, v_tgt;
+  View q_ref, k_fresh, v_fresh, k_cache, v_cache;
+  View o_tgt, o_ref;        // written through const_cast
+  float* mass_tgt;          // [B, H, n_tgt] or null
+  float* lse_tgt;           // [B, H, n_tgt, 2] or null
+  float* mass_refq;         // [B, H, n_ref] or null
+  const int32_t* decision;  // KV_DEVICE only
+  int32_t B, H, n_ref, n_tgt;
+  int32_t qt_ref;       // query tiles per (b, h) over reference rows (0 when they do not attend)
+  int32_t qt_tgt;       // query tiles per (b, h) over target rows
+  int32_t total_tiles;  // B * H * (qt_ref + qt_tgt) = grid size
+  int32_t kvsrc;
+  float sc_log2;  // softmax scale * log2(e)
+};
+
+// Query rows per workgroup of each attention kernel (the host sizes the grid with these).
+constexpr int kAttnBf16BM = 128;
+constexpr int kAttnF32BM = 64;
+
+hipError_t launch_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_attn_f32(const AttnParams& p, int head_dim, hipStream_t stream);
+
+int q_change_chunks(int32_t n_tgt, int32_t head_dim);
+hipError_t launch_q_change(int dtype, int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim, View cur, View prev,
+                           float eps, float* d_out, void* ws, hipStream_t stream);
+
+struct GateState {
+  int32_t reactivated, a_full, delta_max, step;
+};
+hipError_t launch_gate(int32_t B, int32_t H, int32_t n_tgt, int32_t block, int32_t step, int32_t mode,
+                       const float* d_cur, const float* mass_prev, const float* theta, GateState* state,
+                       int32_t* decision_out, float* score_out, hipStream_t stream);
+
+hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, View k_src,
+                               View v_src, View k_dst, View v_dst, const int32_t* decision, int32_t* age,
+                               int32_t step, hipStream_t stream);
+
+// Launches `kernel` and returns the status of THIS launch (hipLaunchKernel's
+// return value), not a sticky error left by earlier runtime calls. Arguments
+// are converted to the kernel's parameter types before their addresses are
+// taken.
+template <typename... KArgs, typename... Args>
+hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem, hipStream_t stream,
+                         Args... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel arity mismatch");
+  std::tuple<KArgs...> held(static_cast<KArgs>(args)...);
+  void* ptrs[sizeof...(KArgs) > 0 ? sizeof...(KArgs) : 1];
+  std::apply(
+      [&](auto&... e) {
+        size_t i = 0;
+        ((ptrs[i++] = static_cast<void*>(&e)), ...);
+      },
+      held);
+  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, shmem, stream);
+}
+
+// Maps a launch index to a tile index so that the workgroups the hardware
+// sends to one XCD (round-robin over the 8 XCDs by launch index) get one
+// contiguous range of tiles; consecutive tiles share (batch, head), so their
+// K/V tiles are re-read from that XCD's L2. A bijection on [0, total).
+__device__ __forceinline__ int xcd_remap(int w, int total) {
+  const int per = total >> 3, rem = total & 7;
+  const int xcd = w & 7, k = w >> 3;
+  return xcd * per + (xcd < rem ? xcd : rem) + k;
+}
+
+}  // namespace refadapt

@@ -1,0 +1,248 @@
+// Controller statistics and cache maintenance (gfx950):
+//   q_change  - relative Frobenius change of the target queries per (b, h)
+//               (paper Sec. 3.1 consecutive-drift equation on post-RoPE target Q)
+//   gate      - head-mean interaction score and the block decision
+//               (Sec. 4 factorized-risk and depth-cutoff equations; Alg. 1)
+//   commit    - device-conditional refresh of a block's reference K/V cache
+//
+// All three are bandwidth- or latency-bound; they use 16-byte coalesced loads
+// and fixed-order reductions, so every result is bitwise reproducible.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "internal.h"
+
+namespace refadapt {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int QC_THREADS = 256;
+constexpr int QC_TARGET_ELEMS = 16384;  // elements of one tensor per workgroup (32 KiB of bf16)
+constexpr int QC_MAX_CHUNKS = 64;
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Fixed-order wavefront reduction (butterfly over the 64 lanes).
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Pass 1: one workgroup sums (cur - prev)^2 and prev^2 over a chunk of rows of one (b, h).
+template <bool BF16>
+__global__ __launch_bounds__(QC_THREADS) void q_change_partial(View cur, View prev, int32_t H, int32_t n_rows,
+                                                               int32_t head_dim, int32_t chunks, float2* ws) {
+  const int bh = blockIdx.y;
+  const int b = bh / H, h = bh - b * H;
+  const int rows_per = (n_rows + chunks - 1) / chunks;
+  const int r0 = blockIdx.x * rows_per;
+  const int r1 = min(n_rows, r0 + rows_per);
+  const int vec = BF16 ? 8 : 4;  // elements per 16-byte load
+  const int vpr = head_dim / vec;
+  const int nvec = max(0, r1 - r0) * vpr;
+  const char* cb = static_cast<const char*>(cur.p);
+  const char* pb = static_cast<const char*>(prev.p);
+  const int esz = BF16 ? 2 : 4;
+  const int64_t cbase = (b * cur.sb + h * cur.sh) * esz;
+  const int64_t pbase = (b * prev.sb + h * prev.sh) * esz;
+
+  float sd = 0.f, sp = 0.f;
+  for (int v = threadIdx.x; v < nvec; v += QC_THREADS) {
+    const int row = r0 + v / vpr, col = (v % vpr) * vec;
+    const u32x4 x = *reinterpret_cast<const u32x4*>(cb + cbase + ((int64_t)row * cur.ss + col) * esz);
+    const u32x4 y = *reinterpret_cast<const u32x4*>(pb + pbase + ((int64_t)row * prev.ss + col) * esz);
+    if (BF16) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float a0 = bf16_lo(x[i]), a1 = bf16_hi(x[i]);
+        const float p0 = bf16_lo(y[i]), p1 = bf16_hi(y[i]);
+        const float d0 = a0 - p0, d1 = a1 - p1;
+        sd = fmaf(d0, d0, sd);
+        sd = fmaf(d1, d1, sd);
+        sp = fmaf(p0, p0, sp);
+        sp = fmaf(p1, p1, sp);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float a = __uint_as_float(x[i]), pp = __uint_as_float(y[i]);
+        const float d = a - pp;
+        sd = fmaf(d, d, sd);
+        sp = fmaf(pp, pp, sp);
+      }
+    }
+  }
+  sd = wave_sum(sd);
+  sp = wave_sum(sp);
+  __shared__ float red[2][QC_THREADS / 64];
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][wave] = sd;
+    red[1][wave] = sp;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float a = 0.f, c = 0.f;
+#pragma unroll
+    for (int w = 0; w < QC_THREADS / 64; ++w) {
+      a += red[0][w];
+      c += red[1][w];
+    }
+    ws[(int64_t)bh * chunks + blockIdx.x] = make_float2(a, c);
+  }
+}
+
+// Pass 2: per (b, h), add the chunk partials in order (fp64) and form D.
+__global__ __launch_bounds__(256) void q_change_final(const float2* ws, int32_t bh_total, int32_t chunks, float eps,
+                                                      float* out) {
+  const int bh = blockIdx.x * blockDim.x + threadIdx.x;
+  if (bh >= bh_total) return;
+  double a = 0.0, c = 0.0;
+  for (int i = 0; i < chunks; ++i) {
+    const float2 v = ws[(int64_t)bh * chunks + i];
+    a += v.x;
+    c += v.y;
+  }
+  out[bh] = (float)(sqrt(a) / (sqrt(c) + (double)eps));
+}
+
+constexpr int GATE_THREADS = 1024;
+
+__global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t n_tgt, int32_t block, int32_t step,
+                                                            int32_t mode, const float* d_cur, const float* mass_prev,
+                                                            const float* theta, GateState* st, int32_t* decision_out,
+                                                            float* score_out) {
+  extern __shared__ float m_head[];  // [BH] mean lagged mass per (b, h)
+  __shared__ int s_react;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  if (tid == 0) {
+    if (block == 0) {  // step bookkeeping of Alg. 1: full refresh at step 0 and after delta_max steps
+      const bool full = step == 0 || (st->delta_max > 0 && step - st->a_full >= st->delta_max);
+      if (full) st->a_full = step;
+      st->reactivated = full ? 1 : 0;
+      st->step = step;
+    }
+    s_react = st->reactivated;
+  }
+
+  // Mean over target queries of the lagged per-query reference mass, one wavefront per (b, h).
+  for (int bh = wave; bh < BH; bh += GATE_THREADS / 64) {
+    const float* row = mass_prev + (int64_t)bh * n_tgt;
+    float s = 0.f;
+    for (int i = lane; i < n_tgt; i += 64) s += row[i];
+    s = wave_sum(s);
+    if (lane == 0) m_head[bh] = s / (float)n_tgt;
+  }
+  __syncthreads();
+
+  if (tid == 0) {
+    double sd = 0.0, sm = 0.0, sg = 0.0;
+    for (int i = 0; i < BH; ++i) {
+      const double d = d_cur[i], m = m_head[i];
+      sd += d;
+      sm += m;
+      sg += d * m;  // per-head product before the mean
+    }
+    const double dm = sd / BH, mm = sm / BH, gm = sg / BH;
+    int dec;
+    if (s_react) {
+      dec = DEC_COMPUTE;
+    } else {
+      bool cross;
+      if (mode == 0) {
+        cross = gm >= (double)theta[block];
+      } else if (mode == 1) {
+        cross = dm >= (double)theta[block];
+      } else if (mode == 2) {
+        cross = mm >= (double)theta[block];
+      } else {
+        cross = dm >= (double)theta[2 * block] && mm >= (double)theta[2 * block + 1];
+      }
+      dec = cross ? DEC_REACTIVATE : DEC_REUSE;
+      if (cross) st->reactivated = 1;
+    }
+    *decision_out = dec;
+    score_out[0] = (float)dm;
+    score_out[1] = (float)mm;
+    score_out[2] = (float)gm;
+  }
+}
+
+constexpr int CC_THREADS = 256;
+
+__global__ __launch_bounds__(CC_THREADS) void cache_commit_kernel(View ks, View vs, View kd, View vd, int32_t H,
+                                                                  int32_t n_rows, int32_t vpr, int32_t esz,
+                                                                  const int32_t* decision, int32_t* age, int32_t step) {
+  if (decision && *decision != DEC_COMPUTE) return;
+  const int bh = blockIdx.y;
+  const int b = bh / H, h = bh - b * H;
+  const int64_t nvec = (int64_t)n_rows * vpr;
+  const int vec = 16 / esz;
+  for (int64_t v = (int64_t)blockIdx.x * CC_THREADS + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * CC_THREADS) {
+    const int64_t row = v / vpr;
+    const int col = (int)(v % vpr) * vec;
+    const int64_t so_k = ((b * ks.sb + h * ks.sh) + row * ks.ss + col) * esz;
+    const int64_t so_v = ((b * vs.sb + h * vs.sh) + row * vs.ss + col) * esz;
+    const int64_t do_k = ((b * kd.sb + h * kd.sh) + row * kd.ss + col) * esz;
+    const int64_t do_v = ((b * vd.sb + h * vd.sh) + row * vd.ss + col) * esz;
+    const u32x4 xk = *reinterpret_cast<const u32x4*>(static_cast<const char*>(ks.p) + so_k);
+    const u32x4 xv = *reinterpret_cast<const u32x4*>(static_cast<const char*>(vs.p) + so_v);
+    *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(kd.p)) + do_k) = xk;
+    *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(vd.p)) + do_v) = xv;
+  }
+  if (age && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *age = step;
+}
+
+}  // namespace
+
+int q_change_chunks(int32_t n_tgt, int32_t head_dim) {
+  const int64_t elems = (int64_t)n_tgt * head_dim;
+  int64_t c = (elems + QC_TARGET_ELEMS - 1) / QC_TARGET_ELEMS;
+  if (c < 1) c = 1;
+  if (c > QC_MAX_CHUNKS) c = QC_MAX_CHUNKS;
+  if (c > n_tgt) c = n_tgt;
+  return (int)c;
+}
+
+hipError_t launch_q_change(int dtype, int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim, View cur, View prev,
+                           float eps, float* d_out, void* ws, hipStream_t stream) {
+  const int chunks = q_change_chunks(n_tgt, head_dim);
+  const dim3 grid(chunks, B * H);
+  float2* w = static_cast<float2*>(ws);
+  const hipError_t e =
+      dtype == 0
+          ? launch_kernel(q_change_partial<true>, grid, dim3(QC_THREADS), 0, stream, cur, prev, H, n_tgt, head_dim,
+                          chunks, w)
+          : launch_kernel(q_change_partial<false>, grid, dim3(QC_THREADS), 0, stream, cur, prev, H, n_tgt, head_dim,
+                          chunks, w);
+  if (e != hipSuccess) return e;
+  const int bh = B * H;
+  return launch_kernel(q_change_final, dim3((bh + 255) / 256), dim3(256), 0, stream, w, bh, chunks, eps, d_out);
+}
+
+hipError_t launch_gate(int32_t B, int32_t H, int32_t n_tgt, int32_t block, int32_t step, int32_t mode,
+                       const float* d_cur, const float* mass_prev, const float* theta, GateState* state,
+                       int32_t* decision_out, float* score_out, hipStream_t stream) {
+  const int bh = B * H;
+  return launch_kernel(gate_kernel, dim3(1), dim3(GATE_THREADS), bh * sizeof(float), stream, bh, n_tgt, block, step,
+                       mode, d_cur, mass_prev, theta, state, decision_out, score_out);
+}
+
+hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, View k_src,
+                               View v_src, View k_dst, View v_dst, const int32_t* decision, int32_t* age,
+                               int32_t step, hipStream_t stream) {
+  const int esz = dtype == 0 ? 2 : 4;
+  const int vpr = head_dim * esz / 16;
+  const int64_t nvec = (int64_t)n_ref * vpr;
+  int gx = (int)((nvec + CC_THREADS * 4 - 1) / (CC_THREADS * 4));
+  if (gx < 1) gx = 1;
+  if (gx > 1024) gx = 1024;
+  return launch_kernel(cache_commit_kernel, dim3(gx, B * H), dim3(CC_THREADS), 0, stream, k_src, v_src, k_dst, v_dst,
+                       H, n_ref, vpr, esz, decision, age, step);
+}
+
+}  // namespace refadapt

@@ -1,0 +1,220 @@
+"""Torch-tensor wrappers over the C ABI (device memory and streams only).
+
+Each function checks devices, dtypes and layouts, allocates outputs with
+torch (caching allocator) when the caller does not pass them, and calls the
+C entry point of the same role on ``torch.cuda.current_stream()``. No torch
+compute op runs on these paths; a tensor that is not on a GPU is an error.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+from . import _lib as L
+
+_DTYPES = {torch.bfloat16: L.RA_BF16, torch.float32: L.RA_F32}
+_QSET = {"target": L.RA_Q_TARGET, "all": L.RA_Q_ALL}
+_KVSRC = {"fresh": L.RA_KV_FRESH, "cache": L.RA_KV_CACHE, "device": L.RA_KV_DEVICE}
+_GATE = {"product": L.RA_GATE_PRODUCT, "q_only": L.RA_GATE_Q_ONLY, "mass_only": L.RA_GATE_MASS_ONLY, "and": L.RA_GATE_AND}
+
+REUSE, REACTIVATE, COMPUTE = L.RA_REUSE, L.RA_REACTIVATE, L.RA_COMPUTE
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _on_gpu(name, t):
+    if t is not None and not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor (the HIP library is the only implementation)")
+
+
+def _view(name, t, dtype=None, shape=None):
+    if t is None:
+        return L.ra_tensor()
+    _on_gpu(name, t)
+    if t.dim() != 4:
+        raise ValueError(f"{name} must be [B, H, S, d], got {tuple(t.shape)}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)} != {tuple(shape)}")
+    if t.numel() == 0:  # an empty segment is never read: pass a null view
+        return L.ra_tensor()
+    if t.stride(-1) != 1:
+        raise ValueError(f"{name}: the head dimension must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype} differs from {dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)} != {tuple(shape)}")
+    return L.ra_tensor(t.data_ptr(), t.stride(0), t.stride(1), t.stride(2))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+@dataclass
+class AttnOut:
+    o_tgt: torch.Tensor
+    o_ref: Optional[torch.Tensor]
+    ref_mass: Optional[torch.Tensor]
+    lse: Optional[torch.Tensor]
+    ref_mass_refq: Optional[torch.Tensor]
+
+
+def joint_attn(
+    q_tgt,
+    k_tgt,
+    v_tgt,
+    *,
+    q_ref=None,
+    k_ref=None,
+    v_ref=None,
+    k_cache=None,
+    v_cache=None,
+    qset="target",
+    kvsrc="fresh",
+    decision=None,
+    scale=None,
+    n_ref=None,
+    o_tgt=None,
+    o_ref=None,
+    ref_mass=True,
+    lse=False,
+    ref_mass_refq=False,
+):
+    """Joint attention over [K_R; K_Y] through ``refadapt_joint_attn``.
+
+    ``ref_mass``/``lse``/``ref_mass_refq`` may be booleans (allocate when True)
+    or preallocated fp32 tensors. Returns an ``AttnOut``.
+    """
+    B, H, n_tgt, D = q_tgt.shape
+    dt = q_tgt.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    if n_ref is None:
+        src = next((t for t in (k_ref, k_cache, q_ref) if t is not None), None)
+        n_ref = 0 if src is None else src.shape[2]
+    dev = q_tgt.device
+    device_mode = kvsrc == "device"
+    ref_queries = (device_mode or qset == "all") and n_ref > 0
+    if o_tgt is None:
+        o_tgt = torch.empty((B, H, n_tgt, D), dtype=dt, device=dev)
+    if ref_queries and o_ref is None:
+        o_ref = torch.empty((B, H, n_ref, D), dtype=dt, device=dev)
+
+    def _opt(flag, shape):
+        if flag is True:
+            return torch.empty(shape, dtype=torch.float32, device=dev)
+        if flag is False or flag is None:
+            return None
+        if flag.dtype != torch.float32 or not flag.is_contiguous() or tuple(flag.shape) != shape:
+            raise ValueError(f"output buffer must be contiguous fp32 of shape {shape}")
+        return flag
+
+    mass_t = _opt(ref_mass, (B, H, n_tgt))
+    lse_t = _opt(lse, (B, H, n_tgt, 2))
+    mrq_t = _opt(ref_mass_refq, (B, H, n_ref)) if n_ref > 0 else None
+    if decision is not None:
+        _on_gpu("decision", decision)
+        if decision.dtype != torch.int32:
+            raise ValueError("decision must be an int32 device tensor")
+
+    shp_t = (B, H, n_tgt, D)
+    shp_r = (B, H, n_ref, D)
+    desc = L.ra_attn_desc(B, H, D, n_ref, n_tgt, _DTYPES[dt], float(scale or 0.0), _QSET[qset], _KVSRC[kvsrc])
+    args = L.ra_attn_args(
+        q_tgt=_view("q_tgt", q_tgt, dt, shp_t),
+        k_tgt=_view("k_tgt", k_tgt, dt, shp_t),
+        v_tgt=_view("v_tgt", v_tgt, dt, shp_t),
+        q_ref=_view("q_ref", q_ref, dt, shp_r),
+        k_ref=_view("k_ref", k_ref, dt, shp_r),
+        v_ref=_view("v_ref", v_ref, dt, shp_r),
+        k_cache=_view("k_cache", k_cache, dt, shp_r),
+        v_cache=_view("v_cache", v_cache, dt, shp_r),
+        decision=None if decision is None else decision.data_ptr(),
+        o_tgt=_view("o_tgt", o_tgt, dt, shp_t),
+        o_ref=_view("o_ref", o_ref, dt, shp_r),
+        ref_mass=None if mass_t is None else mass_t.data_ptr(),
+        lse_tgt=None if lse_t is None else lse_t.data_ptr(),
+        ref_mass_refq=None if mrq_t is None else mrq_t.data_ptr(),
+    )
+    L.refadapt_joint_attn(desc, args, _stream())
+    return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t)
+
+
+def q_change_workspace(q_tgt):
+    B, H, n, D = q_tgt.shape
+    nbytes = L.refadapt_q_change_workspace_size(B, H, n, D)
+    return torch.empty(max(nbytes, 8), dtype=torch.uint8, device=q_tgt.device)
+
+
+def q_change(q_cur, q_prev, eps=1e-8, out=None, workspace=None):
+    """D[b, h] = ||Q_cur - Q_prev||_F / (||Q_prev||_F + eps) through ``refadapt_q_change``."""
+    B, H, n, D = q_cur.shape
+    dt = q_cur.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    if out is None:
+        out = torch.empty((B, H), dtype=torch.float32, device=q_cur.device)
+    if workspace is None:
+        workspace = q_change_workspace(q_cur)
+    _on_gpu("out", out)
+    _on_gpu("workspace", workspace)
+    L.refadapt_q_change(
+        B, H, n, D, _DTYPES[dt],
+        _view("q_cur", q_cur, dt), _view("q_prev", q_prev, dt, q_cur.shape),
+        float(eps), _ptr(out), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(),
+    )
+    return out
+
+
+def new_gate_state(device, delta_max=0):
+    """Device-resident ra_gate_state {reactivated, a_full, delta_max, step} (int32[4])."""
+    return torch.tensor([0, 0, int(delta_max or 0), 0], dtype=torch.int32, device=device)
+
+
+def gate(d_cur, mass_prev, theta, state, block, step, mode="product", decision_out=None, score_out=None):
+    """One block's decision through ``refadapt_gate``; returns (decision int32[1], scores fp32[3])."""
+    B, H = d_cur.shape
+    n_tgt = mass_prev.shape[-1]
+    dev = d_cur.device
+    for name, t in (("d_cur", d_cur), ("mass_prev", mass_prev), ("theta", theta), ("state", state)):
+        _on_gpu(name, t)
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if tuple(mass_prev.shape) != (B, H, n_tgt) or mass_prev.dtype != torch.float32 or d_cur.dtype != torch.float32:
+        raise ValueError("d_cur must be fp32 [B, H] and mass_prev fp32 [B, H, n_tgt]")
+    if theta.dtype != torch.float32 or state.dtype != torch.int32 or state.numel() != 4:
+        raise ValueError("theta must be fp32 and state int32[4]")
+    need = 2 * (block + 1) if mode == "and" else block + 1
+    if theta.numel() < need:
+        raise ValueError(f"theta has {theta.numel()} entries; block {block} needs {need}")
+    if decision_out is None:
+        decision_out = torch.empty(1, dtype=torch.int32, device=dev)
+    if score_out is None:
+        score_out = torch.empty(3, dtype=torch.float32, device=dev)
+    L.refadapt_gate(
+        B, H, n_tgt, int(block), int(step), _GATE[mode],
+        _ptr(d_cur), _ptr(mass_prev), _ptr(theta), _ptr(state), _ptr(decision_out), _ptr(score_out), _stream(),
+    )
+    return decision_out, score_out
+
+
+def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0):
+    """Copy fresh reference K/V into the cache when ``decision`` is COMPUTE (or None)."""
+    B, H, n_ref, D = k_ref.shape
+    dt = k_ref.dtype
+    for name, t in (("decision", decision), ("age", age)):
+        _on_gpu(name, t)
+        if t is not None and t.dtype != torch.int32:
+            raise ValueError(f"{name} must be int32")
+    L.refadapt_cache_commit(
+        B, H, n_ref, D, _DTYPES[dt],
+        _view("k_ref", k_ref, dt), _view("v_ref", v_ref, dt, k_ref.shape),
+        _view("k_cache", k_cache, dt, k_ref.shape), _view("v_cache", v_cache, dt, k_ref.shape),
+        _ptr(decision), _ptr(age), int(step), _stream(),
+    )

@@ -1,0 +1,100 @@
+"""The C-ABI library loads on a host without a GPU, exports every symbol the
+header declares, and rejects malformed arguments before touching a device."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_32415_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "refadapt.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(refadapt_\w+)\s*\(", text)))
+
+
+def test_header_symbols_are_exported():
+    names = _declared()
+    assert set(names) == set(L.EXPORTED)
+    raw = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_version():
+    assert "gfx950" in L.refadapt_version()
+
+
+def _t(ptr=0x1000, sb=0, sh=0, ss=128):
+    return L.ra_tensor(ptr, sb, sh, ss)
+
+
+def _desc(**kw):
+    d = dict(batch=1, heads=2, head_dim=128, n_ref=64, n_tgt=64, dtype=L.RA_BF16, scale=0.0, qset=L.RA_Q_TARGET, kvsrc=L.RA_KV_FRESH)
+    d.update(kw)
+    return L.ra_attn_desc(**d)
+
+
+def _args(**kw):
+    a = dict(q_tgt=_t(), k_tgt=_t(), v_tgt=_t(), o_tgt=_t(), k_ref=_t(), v_ref=_t())
+    a.update(kw)
+    return L.ra_attn_args(**a)
+
+
+@pytest.mark.parametrize(
+    "desc,args,status,msg",
+    [
+        (dict(head_dim=96), {}, L.RA_EUNSUPPORTED, "head_dim"),
+        (dict(n_tgt=0), {}, L.RA_EINVAL, "n_tgt"),
+        (dict(n_ref=-1), {}, L.RA_EINVAL, "n_ref"),
+        (dict(dtype=7), {}, L.RA_EINVAL, "dtype"),
+        (dict(qset=5), {}, L.RA_EINVAL, "qset"),
+        (dict(kvsrc=9), {}, L.RA_EINVAL, "kvsrc"),
+        ({}, dict(q_tgt=_t(0)), L.RA_EINVAL, "q_tgt"),
+        ({}, dict(k_ref=_t(0)), L.RA_EINVAL, "k_ref"),
+        (dict(kvsrc=L.RA_KV_CACHE), {}, L.RA_EINVAL, "k_cache"),
+        (dict(qset=L.RA_Q_ALL), {}, L.RA_EINVAL, "q_ref"),
+        (dict(kvsrc=L.RA_KV_DEVICE), dict(k_cache=_t(), v_cache=_t(), q_ref=_t(), o_ref=_t()), L.RA_EINVAL, "decision"),
+        ({}, dict(q_tgt=_t(ss=132)), L.RA_EUNSUPPORTED, "q_tgt"),
+        ({}, dict(v_tgt=_t(ptr=0x1002)), L.RA_EUNSUPPORTED, "v_tgt"),
+        ({}, dict(k_tgt=_t(ss=64)), L.RA_EINVAL, "row stride"),
+        (dict(batch=0), {}, L.RA_EINVAL, "batch"),
+    ],
+)
+def test_joint_attn_rejects_bad_arguments(desc, args, status, msg):
+    st = L.LIB.refadapt_joint_attn(ctypes.byref(_desc(**desc)), ctypes.byref(_args(**args)), None)
+    assert st == status
+    assert msg in L.refadapt_last_error()
+    with pytest.raises(L.RefadaptError):
+        L.refadapt_joint_attn(_desc(**desc), _args(**args), None)
+
+
+def test_joint_attn_null_structs():
+    assert L.LIB.refadapt_joint_attn(None, None, None) == L.RA_EINVAL
+
+
+def test_q_change_validation():
+    ws = L.refadapt_q_change_workspace_size(1, 24, 4096, 128)
+    assert ws >= 24 * 8 and ws % 8 == 0
+    assert L.refadapt_q_change_workspace_size(0, 1, 1, 1) == 0
+    st = L.LIB.refadapt_q_change(1, 24, 4096, 128, L.RA_BF16, _t(), _t(), 1e-8, ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000), ws - 8, None)
+    assert st == L.RA_EWORKSPACE
+    st = L.LIB.refadapt_q_change(1, 24, 4096, 128, L.RA_BF16, _t(), _t(0), 1e-8, ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000), ws, None)
+    assert st == L.RA_EINVAL and "q_prev" in L.refadapt_last_error()
+    st = L.LIB.refadapt_q_change(1, 24, 4096, 128, L.RA_BF16, _t(), _t(), -1.0, ctypes.c_void_p(0x1000), ctypes.c_void_p(0x2000), ws, None)
+    assert st == L.RA_EINVAL and "eps" in L.refadapt_last_error()
+
+
+def test_gate_and_commit_validation():
+    p = ctypes.c_void_p(0x1000)
+    assert L.LIB.refadapt_gate(1, 24, 4096, 0, 0, 9, p, p, p, p, p, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_gate(1, 24, 4096, -1, 0, 0, p, p, p, p, p, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_gate(1, 24, 4096, 0, 0, 0, None, p, p, p, p, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_cache_commit(1, 2, 10, 128, L.RA_BF16, _t(), _t(), _t(0), _t(), None, None, 0, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_cache_commit(1, 2, 10, 100, L.RA_BF16, _t(), _t(), _t(), _t(), None, None, 0, None) == L.RA_EUNSUPPORTED
+    # Nothing to copy is not an error.
+    assert L.LIB.refadapt_cache_commit(1, 2, 0, 128, L.RA_BF16, _t(), _t(), _t(), _t(), None, None, 0, None) == L.RA_OK

@@ -1,0 +1,204 @@
+"""GPU parity of refadapt_joint_attn against the fp64 oracle (through the C ABI).
+
+Small cases compare every output element; shapes span several query and key
+tiles and end in ragged tails. Full-size workloads compare sampled query rows
+(each row of softmax attention is independent, so a sampled row is an exact
+check of that row).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import MASS_TOL, O_TOL, dev, host, max_abs
+from oracle import joint_attention
+from paper_2609_32415_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ops = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _ops():
+    global ops
+    from paper_2609_32415_amd import ops as _o
+
+    ops = _o
+    yield
+
+
+def _inputs(dtype, d, n_ref, n_tgt, B=1, H=2, seed=7, bias=True):
+    base = "tiny" if dtype == "f32" else "single_ref"
+    w = synth.workload(base, batch=B, heads=H, head_dim=d, n_ref=n_ref, n_tgt=n_tgt, seed=seed,
+                       key_bias=bias and H > 1, cache_noise=0.01)
+    x = synth.block_inputs(w)
+    x.update({f"{k}_cache": v for k, v in synth.stale_cache(w, x).items()})
+    return w, x
+
+
+def _oracle(x, qset, use_cache, scale=None):
+    kr = x["k_ref_cache"] if use_cache else x["k_ref"]
+    vr = x["v_ref_cache"] if use_cache else x["v_ref"]
+    n_ref = x["k_ref"].shape[2]
+    res = {"tgt": joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"], scale)}
+    if qset == "all" and n_ref > 0:
+        res["ref"] = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"], scale)
+    return res
+
+
+def _gpu(x, dtype, qset, kvsrc, **kw):
+    t = {k: dev(v, dtype) for k, v in x.items()}
+    n_ref = x["k_ref"].shape[2]
+    out = ops.joint_attn(
+        t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
+        k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], qset=qset, kvsrc=kvsrc, n_ref=n_ref,
+        lse=True, ref_mass_refq=True, **kw,
+    )
+    torch.cuda.synchronize()
+    return out
+
+
+SMALL = [
+    # dtype, d, n_ref, n_tgt, B, H
+    ("bf16", 128, 200, 333, 2, 3),
+    ("bf16", 128, 64, 128, 1, 2),
+    ("bf16", 128, 1, 1, 1, 2),
+    ("bf16", 128, 129, 257, 1, 2),
+    ("bf16", 128, 0, 130, 1, 2),
+    ("bf16", 64, 200, 333, 1, 3),
+    ("f32", 64, 256, 256, 1, 2),
+    ("f32", 64, 100, 77, 2, 2),
+    ("f32", 128, 70, 90, 1, 2),
+    ("f32", 64, 0, 65, 1, 1),
+]
+MODES = [("target", "fresh"), ("target", "cache"), ("all", "fresh"), ("all", "cache")]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: "-".join(map(str, c)))
+@pytest.mark.parametrize("mode", MODES, ids=lambda m: "/".join(m))
+def test_small_parity_all_elements(case, mode):
+    dtype, d, n_ref, n_tgt, B, H = case
+    qset, kvsrc = mode
+    print(f"case {case} mode {mode}", flush=True)
+    _, x = _inputs(dtype, d, n_ref, n_tgt, B, H)
+    got = _gpu(x, dtype, qset, kvsrc)
+    ref = _oracle(x, qset, kvsrc == "cache")
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL[dtype]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL[dtype]
+    lse = host(got.lse)
+    assert max_abs(lse[..., 1], ref["tgt"]["lse_all"]) <= 1e-3
+    if n_ref > 0:
+        assert max_abs(lse[..., 0], ref["tgt"]["lse_ref"]) <= 1e-3
+    else:
+        assert np.all(np.isneginf(lse[..., 0]))
+        assert np.all(host(got.ref_mass) == 0.0)
+    m = host(got.ref_mass)
+    assert np.all((m >= 0) & (m <= 1))
+    if qset == "all" and n_ref > 0:
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL[dtype]
+        assert max_abs(host(got.ref_mass_refq), ref["ref"]["ref_mass"]) <= MASS_TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+@pytest.mark.parametrize("decision", [0, 1, 2], ids=["REUSE", "REACTIVATE", "COMPUTE"])
+def test_device_mode_follows_decision_word(dtype, d, decision):
+    print(f"device mode {dtype} d{d} decision {decision}", flush=True)
+    _, x = _inputs(dtype, d, 150, 190, 1, 2)
+    sentinel = 7.0
+    o_ref = torch.full((1, 2, 150, d), sentinel, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device="cuda:0")
+    dec = torch.tensor([decision], dtype=torch.int32, device="cuda:0")
+    got = _gpu(x, dtype, "target", "device", decision=dec, o_ref=o_ref)
+    use_cache = decision != 2
+    ref = _oracle(x, "all", use_cache)
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL[dtype]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL[dtype]
+    if decision == 0:
+        assert np.all(host(o_ref) == sentinel)  # reference rows skipped on a reused block
+    else:
+        assert max_abs(host(o_ref), ref["ref"]["o"]) <= O_TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_invariants_rows_sum_to_one_and_indicator_gives_mass(dtype, d):
+    _, x = _inputs(dtype, d, 190, 230, 1, 3)
+    ones = dict(x, v_ref=np.ones_like(x["v_ref"]), v_tgt=np.ones_like(x["v_tgt"]))
+    got = _gpu(ones, dtype, "all", "fresh")
+    assert max_abs(host(got.o_tgt), 1.0) <= (O_TOL["bf16"] if dtype == "bf16" else 1e-6)
+    assert max_abs(host(got.o_ref), 1.0) <= (O_TOL["bf16"] if dtype == "bf16" else 1e-6)
+    ind = dict(x, v_ref=np.ones_like(x["v_ref"]), v_tgt=np.zeros_like(x["v_tgt"]))
+    got = _gpu(ind, dtype, "target", "fresh")
+    o = host(got.o_tgt)
+    m = host(got.ref_mass)
+    assert max_abs(o, np.broadcast_to(m[..., None], o.shape)) <= (1e-2 if dtype == "bf16" else 1e-6)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_unchanged_cache_equals_full_fresh_target_rows(dtype, d):
+    """Reuse with cache == fresh reproduces the full-fresh target rows bit for bit."""
+    _, x = _inputs(dtype, d, 200, 260, 1, 2)
+    same = dict(x, k_ref_cache=x["k_ref"], v_ref_cache=x["v_ref"])
+    reuse = _gpu(same, dtype, "target", "cache")
+    full = _gpu(same, dtype, "all", "fresh")
+    assert torch.equal(reuse.o_tgt, full.o_tgt)
+    assert torch.equal(reuse.ref_mass, full.ref_mass)
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("f32", 64)])
+def test_mass_outputs_do_not_change_o_and_runs_are_deterministic(dtype, d):
+    _, x = _inputs(dtype, d, 130, 300, 1, 2)
+    t = {k: dev(v, dtype) for k, v in x.items()}
+    kw = dict(k_ref=t["k_ref"], v_ref=t["v_ref"], qset="target", kvsrc="fresh")
+    a = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], ref_mass=False, lse=False, **kw)
+    b = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], ref_mass=True, lse=True, **kw)
+    c = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], ref_mass=True, lse=True, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(a.o_tgt, b.o_tgt)
+    assert torch.equal(b.o_tgt, c.o_tgt) and torch.equal(b.ref_mass, c.ref_mass) and torch.equal(b.lse, c.lse)
+
+
+def test_custom_scale_and_strided_views():
+    """A non-default scale and non-contiguous [B, S, H, d] views (head-interleaved layout)."""
+    _, x = _inputs("bf16", 128, 96, 200, 1, 2)
+    ref = _oracle(x, "target", False, scale=0.05)
+    t = {k: dev(v, "bf16").transpose(1, 2).contiguous().transpose(1, 2) for k, v in x.items()}
+    assert t["q_tgt"].stride(1) == 128
+    got = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=t["k_ref"], v_ref=t["v_ref"], scale=0.05)
+    torch.cuda.synchronize()
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+
+
+FULL = [("single_ref", "target", "cache"), ("single_ref", "all", "fresh"), ("multi_ref", "target", "cache"),
+        ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"), ("video", "target", "cache")]
+_FULL_CACHE = {}
+
+
+def _full_inputs(name):
+    if name not in _FULL_CACHE:
+        _FULL_CACHE.clear()
+        w = synth.workload(name)
+        x = synth.block_inputs(w)
+        x.update({f"{k}_cache": v for k, v in synth.stale_cache(w, x).items()})
+        _FULL_CACHE[name] = (w, x)
+    return _FULL_CACHE[name]
+
+
+@pytest.mark.parametrize("name,qset,kvsrc", FULL, ids=lambda v: str(v))
+def test_full_size_sampled_rows(name, qset, kvsrc):
+    print(f"full-size {name} {qset}/{kvsrc}", flush=True)
+    w, x = _full_inputs(name)
+    got = _gpu(x, "bf16", qset, kvsrc)
+    use_cache = kvsrc == "cache"
+    kr = x["k_ref_cache"] if use_cache else x["k_ref"]
+    vr = x["v_ref_cache"] if use_cache else x["v_ref"]
+    rows = synth.sample_rows(w.n_tgt, 48, 3)
+    ref = joint_attention(x["q_tgt"][:, :, rows], kr, vr, x["k_tgt"], x["v_tgt"])
+    assert max_abs(host(got.o_tgt[:, :, rows]), ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass[:, :, rows]), ref["ref_mass"]) <= MASS_TOL["bf16"]
+    m = host(got.ref_mass)
+    assert np.all((m >= 0) & (m <= 1))
+    if qset == "all":
+        rr = synth.sample_rows(w.n_ref, 48, 4)
+        refr = joint_attention(x["q_ref"][:, :, rr], kr, vr, x["k_tgt"], x["v_tgt"])
+        assert max_abs(host(got.o_ref[:, :, rr]), refr["o"]) <= O_TOL["bf16"]

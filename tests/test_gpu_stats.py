@@ -1,0 +1,147 @@
+"""GPU parity of refadapt_q_change, refadapt_gate and refadapt_cache_commit
+against the fp64 oracle (through the C ABI)."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import dev, host
+from oracle import COMPUTE, REACTIVATE, REUSE, gate, q_change
+from oracle.stats import full_refresh_due
+from paper_2609_32415_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ops = None
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _ops():
+    global ops
+    from paper_2609_32415_amd import ops as _o
+
+    ops = _o
+    yield
+
+
+@pytest.mark.parametrize(
+    "dtype,B,H,n,d,sigma",
+    [("f32", 1, 2, 256, 64, 0.3), ("bf16", 1, 24, 4096, 128, 0.3), ("bf16", 2, 3, 333, 128, 0.05),
+     ("bf16", 1, 2, 1, 64, 0.2), ("f32", 1, 1, 7, 128, 1e-3), ("bf16", 1, 24, 16384, 128, 0.2)],
+)
+def test_q_change_parity(dtype, B, H, n, d, sigma):
+    print(f"q_change {dtype} {B}x{H}x{n}x{d}", flush=True)
+    w = synth.workload("tiny", dtype=dtype, batch=B, heads=H, n_ref=1, n_tgt=n, head_dim=d, tgt_drift=sigma)
+    tr = synth.Trajectory(w)
+    prev = tr.step_tensors(0)["q_tgt"]
+    cur = tr.step_tensors(1)["q_tgt"]
+    got = ops.q_change(dev(cur, dtype), dev(prev, dtype), eps=1e-8)
+    torch.cuda.synchronize()
+    ref = q_change(cur, prev, 1e-8)
+    np.testing.assert_allclose(host(got), ref, rtol=1e-5, atol=0)
+
+
+def test_q_change_closed_forms_on_device():
+    q = np.random.default_rng(0).standard_normal((1, 3, 100, 64)).astype(np.float32)
+    z = ops.q_change(dev(q, "f32"), dev(q, "f32"))
+    neg = ops.q_change(dev(-q, "f32"), dev(q, "f32"), eps=0.0)
+    zero_prev = ops.q_change(dev(q, "f32"), dev(np.zeros_like(q), "f32"), eps=1e-3)
+    torch.cuda.synchronize()
+    assert np.all(host(z) == 0)
+    np.testing.assert_allclose(host(neg), 2.0, rtol=1e-6)
+    np.testing.assert_allclose(host(zero_prev), np.sqrt((q.astype(np.float64) ** 2).sum((-2, -1))) / 1e-3, rtol=1e-5)
+
+
+def test_q_change_is_deterministic():
+    w = synth.workload("single_ref", heads=8, n_tgt=4096)
+    x = synth.block_inputs(w)
+    a, b = dev(x["q_tgt"], "bf16"), dev(x["q_ref"][:, :, :4096], "bf16")
+    r1, r2 = ops.q_change(a, b), ops.q_change(a, b)
+    torch.cuda.synchronize()
+    assert torch.equal(r1, r2)
+
+
+NAMES = {REUSE: "REUSE", REACTIVATE: "REACTIVATE", COMPUTE: "COMPUTE"}
+
+
+def _gate_inputs(seed, B, H, n):
+    rng = np.random.default_rng(seed)
+    d = rng.uniform(0.0, 0.6, (B, H)).astype(np.float32)
+    m = rng.uniform(0.0, 1.0, (B, H, n)).astype(np.float32)
+    return d, m
+
+
+@pytest.mark.parametrize("mode", ["product", "q_only", "mass_only", "and"])
+def test_gate_sequence_matches_oracle(mode):
+    """A sequence of steps x blocks of gate calls reproduces the oracle's decisions
+    and scores on identical (D, M) inputs, including the step bookkeeping."""
+    B, H, n, n_blocks, n_steps = 1, 24, 4096, 6, 4
+    rng = np.random.default_rng(1)
+    if mode == "and":
+        th = np.stack([rng.uniform(0.1, 0.4, n_blocks), rng.uniform(0.3, 0.7, n_blocks)], 1).astype(np.float32)
+    elif mode == "product":
+        th = rng.uniform(0.05, 0.2, n_blocks).astype(np.float32)
+    else:
+        th = rng.uniform(0.2, 0.6, n_blocks).astype(np.float32)
+    theta = torch.from_numpy(th.reshape(-1)).cuda()
+    state = ops.new_gate_state("cuda:0", delta_max=3)
+    a_full = 0
+    for t in range(n_steps):
+        full = full_refresh_due(t, a_full, 3)
+        if full:
+            a_full = t
+        react = full
+        for b in range(n_blocks):
+            d, m = _gate_inputs(100 * t + b, B, H, n)
+            dec, score = ops.gate(dev(d, "f32"), dev(m, "f32"), theta, state, b, t, mode)
+            torch.cuda.synchronize()
+            exp = gate(d, m, float(th[b][0] if mode == "and" else th[b]), react, mode=mode,
+                       theta_m=float(th[b][1]) if mode == "and" else None)
+            react = exp.reactivated
+            got = int(dec.item())
+            margin = {"product": exp.g_mean, "q_only": exp.d_mean, "mass_only": exp.m_mean, "and": exp.d_mean}[mode]
+            thr = float(th[b][0] if mode == "and" else th[b])
+            if abs(margin - thr) > 1e-4:
+                assert got == exp.decision, (t, b, NAMES[got], NAMES[exp.decision])
+            else:
+                react = got != REUSE
+            s = host(score)
+            np.testing.assert_allclose(s, [exp.d_mean, exp.m_mean, exp.g_mean], rtol=1e-5, atol=1e-7)
+        st = state.cpu().tolist()
+        assert st[1] == a_full and st[3] == t
+
+
+def test_gate_thresholds_zero_and_infinite():
+    B, H, n = 1, 4, 300
+    d, m = _gate_inputs(5, B, H, n)
+    for thv, expect in ((0.0, REACTIVATE), (math.inf, REUSE)):
+        state = ops.new_gate_state("cuda:0")
+        theta = torch.full((2,), thv, dtype=torch.float32, device="cuda:0")
+        ops.gate(dev(d, "f32"), dev(m, "f32"), theta, state, 0, 1, "product")  # block 0 of step 1
+        dec, _ = ops.gate(dev(d, "f32"), dev(m, "f32"), theta, state, 1, 1, "product")
+        torch.cuda.synchronize()
+        assert int(dec.item()) == (COMPUTE if expect == REACTIVATE else REUSE)
+    # Step 0 computes every block whatever theta says.
+    state = ops.new_gate_state("cuda:0")
+    theta = torch.full((1,), math.inf, dtype=torch.float32, device="cuda:0")
+    dec, _ = ops.gate(dev(d, "f32"), dev(m, "f32"), theta, state, 0, 0, "product")
+    torch.cuda.synchronize()
+    assert int(dec.item()) == COMPUTE
+
+
+@pytest.mark.parametrize("decision,copied", [(2, True), (1, False), (0, False), (None, True)])
+def test_cache_commit(decision, copied):
+    rng = np.random.default_rng(3)
+    shape = (1, 3, 200, 128)
+    src_k, src_v = (dev(rng.standard_normal(shape).astype(np.float32), "bf16") for _ in range(2))
+    ck, cv = torch.zeros_like(src_k), torch.zeros_like(src_v)
+    age = torch.full((1,), -1, dtype=torch.int32, device="cuda:0")
+    dec = None if decision is None else torch.tensor([decision], dtype=torch.int32, device="cuda:0")
+    ops.cache_commit(src_k, src_v, ck, cv, decision=dec, age=age, step=5)
+    torch.cuda.synchronize()
+    if copied:
+        assert torch.equal(ck, src_k) and torch.equal(cv, src_v) and int(age.item()) == 5
+    else:
+        assert torch.count_nonzero(ck) == 0 and torch.count_nonzero(cv) == 0 and int(age.item()) == -1
