@@ -1,23 +1,37 @@
 // Joint attention over [reference; target] keys on bf16 MFMA (gfx950).
 //
 // One workgroup = 4 wavefronts = 128 query rows of one (batch, head); each
-// wavefront owns 32 query rows. Key/value tiles of 64 rows stream through a
-// double-buffered LDS stage, reference tiles first (from the fresh or the
-// cached reference K/V, chosen once per workgroup) and then target tiles.
+// wavefront owns 32 query rows. Key/value tiles of 64 rows stream through LDS,
+// reference tiles first (from the fresh or the cached reference K/V, chosen
+// once per workgroup) and then target tiles.
 //
-// Per tile, a wavefront computes the transposed score block S^T = K Q^T with
-// v_mfma_f32_32x32x16_bf16 (keys on the M side, its 32 queries on the N side),
-// so every lane holds 32 scores of ONE query: the row max and row sum of the
-// online softmax are in-lane reductions plus one exchange with lane l^32. The
-// probabilities P^T stay in registers and feed O^T += V^T P^T directly as the
-// B operand; V^T comes from the LDS stage, where V is stored transposed.
+// Scores are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16
+// (keys on the M side, the wavefront's 32 queries on the N side), so every lane
+// holds 32 scores of ONE query: row max and row sum are in-lane reductions plus
+// one v_permlane32_swap. The probabilities P^T stay in registers and feed
+// O^T += V^T P^T directly as the B operand; the V^T A operand is read from the
+// row-major V tile with ds_read_b64_tr_b16 (LDS transpose read).
 //
-// Split statistics for the reference mass: when the last reference tile is
-// done the running (max, sum) pair is frozen as (m_R, l_R) and the sum restarts
-// at zero for the target tiles, so at the end L_R = l_R * 2^(m_R - m) and
-// L_Y = l are the reference and target parts of the softmax denominator in
-// the same scale; mass = L_R / (L_R + L_Y) lies in [0, 1] by construction and
-// equals exp(lse_R - lse_all) (paper Sec. 3.2 directional exposure).
+// Software pipeline (per wavefront): iteration j issues the 16 MFMAs of S_{j+1}
+// each followed by a slice of the softmax of S_j (phase A), then the 16 MFMAs
+// of O += V_j^T P_j^T, under the first half of which the probabilities of the
+// second half of P_j are formed (phase B). sched_barrier fences keep that
+// order, so the vector ALU works while the matrix core runs. K tiles run one
+// tile ahead of V tiles through two LDS buffers each, refilled from registers
+// loaded at the top of the iteration; one barrier per tile.
+//
+// Online softmax in the exp2 domain with lazy rescaling: a lane moves its
+// running max only when a tile's max exceeds it by more than 2^8, so the O
+// rescale is almost never executed; probabilities are then bounded by 2^8.
+// Row sums add the fp32 probabilities (two chains per lane), so the reference
+// mass and the log-sum-exp carry no bf16 rounding.
+//
+// Split statistics for the reference mass (paper Sec. 3.2, directional
+// exposure): after the last reference tile the running (max, sum) pair is
+// frozen as (m_R, l_R) and the sum restarts at zero, so at the end
+// L_R = l_R * 2^(m_R - m) and L_Y = l are the reference and target parts of
+// the softmax denominator in one scale; mass = L_R / (L_R + L_Y) lies in
+// [0, 1] by construction and equals exp(lse_R - lse_all).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -27,90 +41,106 @@ namespace refadapt {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr int BM = kAttnBf16BM;  // query rows per workgroup
 constexpr int BN = 64;           // keys per LDS tile
 constexpr int NT = 256;          // threads per workgroup
+constexpr float TAU = 8.0f;      // lazy-rescale threshold (log2 units)
 
 // Row permutation of a 32-key MFMA block: swaps bits 2 and 3 of the row index.
-// Loading K row sigma(m) into A-row m makes output register r of lane-half g
-// hold key 16*(r/8) + 8*g + r%8, i.e. eight consecutive keys per lane-half,
-// which is exactly the K-operand order of the next MFMA's B operand (P^T).
+// With key sigma(m) in A-row m of S^T = K Q^T, output register r of lane-half g
+// holds key 16*(r/8) + 8*g + r%8: eight consecutive keys per lane-half, which is
+// exactly the K-operand order of the B operand (P^T) of the PV product.
 __device__ __forceinline__ int sigma(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
 
-__device__ __forceinline__ float wave_xor32_max(float v) { return fmaxf(v, __shfl_xor(v, 32)); }
-__device__ __forceinline__ float wave_xor32_add(float v) { return v + __shfl_xor(v, 32); }
+// max / sum of a value with its partner lane l ^ 32.
+__device__ __forceinline__ float xor32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_add(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
-template <int D>
-struct Prefetch {
-  static constexpr int KCH = D / 8;               // 16-byte chunks per row
-  static constexpr int NK = BN * KCH / NT;        // K chunks per thread
-  static constexpr int NV = (BN / 2) * KCH / NT;  // V (key pair, chunk) units per thread
-  u32x4 k[NK];
-  u32x4 v[2 * NV];
-};
-
-template <int D>
-__device__ __forceinline__ void load_tile(Prefetch<D>& pf, const uint16_t* kb, const uint16_t* vb, int64_t kss,
-                                          int64_t vss, int valid, int tid) {
-  constexpr int KCH = D / 8;
-#pragma unroll
-  for (int i = 0; i < Prefetch<D>::NK; ++i) {
-    const int c = tid + NT * i;
-    const int row = c / KCH, ch = c % KCH;
-    pf.k[i] = row < valid ? *reinterpret_cast<const u32x4*>(kb + row * kss + ch * 8) : u32x4{0, 0, 0, 0};
-  }
-#pragma unroll
-  for (int i = 0; i < Prefetch<D>::NV; ++i) {
-    const int u = tid + NT * i;
-    const int ch = u % KCH, pair = u / KCH;
-    const int r0 = 2 * pair;
-    pf.v[2 * i] = r0 < valid ? *reinterpret_cast<const u32x4*>(vb + r0 * vss + ch * 8) : u32x4{0, 0, 0, 0};
-    pf.v[2 * i + 1] =
-        r0 + 1 < valid ? *reinterpret_cast<const u32x4*>(vb + (r0 + 1) * vss + ch * 8) : u32x4{0, 0, 0, 0};
-  }
+// Keeps a value in a register at this point of the program, so the optimizer
+// cannot sink the instructions that produce it into a later block.
+template <typename T>
+__device__ __forceinline__ void pin(T& v) {
+  asm volatile("" : "+v"(v));
 }
 
 // LDS layouts (bf16 elements):
-//  K  tile: [BN][D], row r, 16-byte chunk c stored at chunk c ^ (sigma(r % 32) % 8)
-//  V^T tile: [D][BN], row d, 16-byte chunk c (8 keys) stored at chunk c ^ ((d ^ (d / 8)) % 8)
-// Both swizzles make the MFMA operand reads and the tile writes free of bank conflicts.
+//   K tile: BN rows of stride D + 8 (row padding of 16 bytes); key r lives in LDS
+//           row sigma(r % 32) + 32 * (r / 32), so A-row m of an S^T block reads
+//           LDS row m. The 16-byte operand reads of 8 consecutive rows then hit
+//           8 distinct bank groups.
+//   V tile: BN rows of stride D + 32 (row padding of 64 bytes): keys of opposite
+//           parity fall in opposite bank halves, which makes the transpose reads
+//           of the V^T operand conflict-free.
 template <int D>
-__device__ __forceinline__ void store_tile(const Prefetch<D>& pf, uint16_t* ks, uint16_t* vts, int tid) {
-  constexpr int KCH = D / 8;
+struct Layout {
+  static constexpr int KROW = D + 8;
+  static constexpr int VROW = D + 32;
+  static constexpr int KTILE = BN * KROW;
+  static constexpr int VTILE = BN * VROW;
+  static constexpr int KCH = D / 8;          // 16-byte chunks per row
+  static constexpr int NCH = BN * KCH / NT;  // chunks per thread per tile
+};
+
+template <int D>
+struct Staging {
+  u32x4 r[Layout<D>::NCH];
+};
+
+// Buffer resource of one K or V tile: base = its first row, range = its valid
+// rows, so loads of rows past a ragged tile's end return zero without a branch.
+// The base and range are workgroup-uniform; readfirstlane states it, so the
+// resource lives in scalar registers.
+template <int D>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base, int64_t ss, int valid) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+  const uint32_t nbytes = __builtin_amdgcn_readfirstlane((uint32_t)((int64_t)(valid - 1) * ss * 2 + D * 2));
+  void* ub = reinterpret_cast<void*>(((uint64_t)hi << 32) | lo);
+  return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, (int)nbytes, 0x00020000);
+}
+
+// Thread t loads 16-byte chunk t % KCH of rows t / KCH + i * (NT / KCH): one
+// per-thread byte offset plus a uniform row step.
+template <int D>
+__device__ __forceinline__ void stage_load(Staging<D>& st, __amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t step) {
 #pragma unroll
-  for (int i = 0; i < Prefetch<D>::NK; ++i) {
-    const int c = tid + NT * i;
-    const int row = c / KCH, ch = c % KCH;
-    const int phys = ch ^ (sigma(row & 31) & 7);
-    *reinterpret_cast<u32x4*>(ks + row * D + phys * 8) = pf.k[i];
-  }
+  for (int i = 0; i < Layout<D>::NCH; ++i)
+    st.r[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff, __builtin_amdgcn_readfirstlane(i * step), 0);
+}
+
+// The matching LDS stores: element offset of the thread's first chunk, then a
+// fixed row step (NT / KCH rows, which sigma leaves in place).
+template <int D, bool IS_K>
+__device__ __forceinline__ void stage_store(const Staging<D>& st, uint16_t* tile, int lds_off) {
+  constexpr int ROW = IS_K ? Layout<D>::KROW : Layout<D>::VROW;
+  constexpr int STEP = (NT / Layout<D>::KCH) * ROW;
 #pragma unroll
-  for (int i = 0; i < Prefetch<D>::NV; ++i) {
-    const int u = tid + NT * i;
-    const int ch = u % KCH, pair = u / KCH;
-    const int key = 2 * pair;
-    const u32x4 a = pf.v[2 * i], b = pf.v[2 * i + 1];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int d = ch * 8 + e;
-      const uint32_t wa = a[e >> 1], wb = b[e >> 1];
-      const uint32_t packed = (e & 1) ? ((wa >> 16) | (wb & 0xffff0000u)) : ((wa & 0xffffu) | (wb << 16));
-      const int phys = (key >> 3) ^ ((d ^ (d >> 3)) & 7);
-      *reinterpret_cast<uint32_t*>(vts + d * BN + phys * 8 + (key & 7)) = packed;
-    }
-  }
+  for (int i = 0; i < Layout<D>::NCH; ++i) *reinterpret_cast<u32x4*>(tile + lds_off + i * STEP) = st.r[i];
 }
 
 template <int D>
-__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
-  constexpr int KS = D / 16;  // MFMA k-steps over the head dim for S^T
-  constexpr int DB = D / 32;  // 32-row blocks of the O^T accumulator
-  constexpr int TILE = BN * D;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2][2 * TILE];
+__global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
+  constexpr int KS = D / 16;   // MFMA k-steps over the head dim for S^T
+  constexpr int DB = D / 32;   // 32-row blocks of the O^T accumulator
+  constexpr int NQK = 2 * KS;  // MFMAs of one S^T tile
+  constexpr int NPV = 4 * DB;  // MFMAs of one PV tile
+  constexpr int KROW = Layout<D>::KROW, VROW = Layout<D>::VROW;
+  __shared__ __attribute__((aligned(16))) uint16_t kbuf[2][Layout<D>::KTILE];
+  __shared__ __attribute__((aligned(16))) uint16_t vbuf[2][Layout<D>::VTILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -137,45 +167,89 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const int n_rows = ref_rows ? p.n_ref : p.n_tgt;
   const View& krv = use_cache ? p.k_cache : p.k_fresh;
   const View& vrv = use_cache ? p.v_cache : p.v_fresh;
-
   const uint16_t* kr = static_cast<const uint16_t*>(krv.p) + b * krv.sb + h * krv.sh;
   const uint16_t* vr = static_cast<const uint16_t*>(vrv.p) + b * vrv.sb + h * vrv.sh;
   const uint16_t* ky = static_cast<const uint16_t*>(p.k_tgt.p) + b * p.k_tgt.sb + h * p.k_tgt.sh;
   const uint16_t* vy = static_cast<const uint16_t*>(p.v_tgt.p) + b * p.v_tgt.sb + h * p.v_tgt.sh;
 
-  // ---- this lane's query row; Q^T as the B operand (query n, head-dim chunk 2*ks + g)
+  const int n_rt = (p.n_ref + BN - 1) / BN;
+  const int n_yt = (p.n_tgt + BN - 1) / BN;
+  const int nt = n_rt + n_yt;
+  auto tile_valid = [&](int j) { return j < n_rt ? min(BN, p.n_ref - j * BN) : min(BN, p.n_tgt - (j - n_rt) * BN); };
+  // Per-thread staging offsets (bytes into a tile, per segment) and LDS offsets.
+  constexpr int KCH = Layout<D>::KCH;
+  const int st_row = tid / KCH, st_ch = tid % KCH;
+  const uint32_t voff_r = (uint32_t)(st_row * krv.ss * 2 + st_ch * 16);
+  const uint32_t voff_rv = (uint32_t)(st_row * vrv.ss * 2 + st_ch * 16);
+  const uint32_t voff_yk = (uint32_t)(st_row * p.k_tgt.ss * 2 + st_ch * 16);
+  const uint32_t voff_yv = (uint32_t)(st_row * p.v_tgt.ss * 2 + st_ch * 16);
+  constexpr int ROWS_PER_STEP = NT / KCH;
+  const int k_st = ((st_row & ~31) | sigma(st_row & 31)) * KROW + st_ch * 8;
+  const int v_st = st_row * VROW + st_ch * 8;
+  auto load_k = [&](Staging<D>& st, int j) {
+    const int valid = tile_valid(j);
+    if (j < n_rt) {
+      stage_load<D>(st, tile_rsrc<D>(kr + (int64_t)j * BN * krv.ss, krv.ss, valid), voff_r,
+                    (uint32_t)(ROWS_PER_STEP * krv.ss * 2));
+    } else {
+      stage_load<D>(st, tile_rsrc<D>(ky + (int64_t)(j - n_rt) * BN * p.k_tgt.ss, p.k_tgt.ss, valid), voff_yk,
+                    (uint32_t)(ROWS_PER_STEP * p.k_tgt.ss * 2));
+    }
+  };
+  auto load_v = [&](Staging<D>& st, int j) {
+    const int valid = tile_valid(j);
+    if (j < n_rt) {
+      stage_load<D>(st, tile_rsrc<D>(vr + (int64_t)j * BN * vrv.ss, vrv.ss, valid), voff_rv,
+                    (uint32_t)(ROWS_PER_STEP * vrv.ss * 2));
+    } else {
+      stage_load<D>(st, tile_rsrc<D>(vy + (int64_t)(j - n_rt) * BN * p.v_tgt.ss, p.v_tgt.ss, valid), voff_yv,
+                    (uint32_t)(ROWS_PER_STEP * p.v_tgt.ss * 2));
+    }
+  };
+
+  // ---- this lane's query row; Q^T as the B operand (query n, head-dim chunk 2*kk + g)
   const int qrow = qt * BM + wave * 32 + n;
   const bool qvalid = qrow < n_rows;
   bf16x8 qreg[KS];
   {
     const uint16_t* qp = static_cast<const uint16_t*>(qv.p) + b * qv.sb + h * qv.sh + (int64_t)qrow * qv.ss;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      u32x4 raw = qvalid ? *reinterpret_cast<const u32x4*>(qp + ks * 16 + g * 8) : u32x4{0, 0, 0, 0};
-      qreg[ks] = __builtin_bit_cast(bf16x8, raw);
+    for (int kk = 0; kk < KS; ++kk) {
+      u32x4 raw = qvalid ? *reinterpret_cast<const u32x4*>(qp + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
+      // Q^T is only ever an MFMA operand: keep it in accumulation registers, which
+      // leaves the vector registers to the two score tiles and the softmax.
+      asm volatile("" : "+a"(raw));
+      qreg[kk] = __builtin_bit_cast(bf16x8, raw);
     }
   }
 
-  const int n_rt = (p.n_ref + BN - 1) / BN;
-  const int n_yt = (p.n_tgt + BN - 1) / BN;
-  const int nt = n_rt + n_yt;
+  // lane-dependent parts of the LDS operand addresses (everything else is an immediate)
+  const int k_lane = n * KROW + 8 * g;           // A-row n, head-dim chunk g
+  const int tr_i = lane & 15, tr_G = lane >> 4;  // 16-lane group of the transpose read
+  const int v_lane = (8 * (tr_G >> 1) + (tr_i >> 2)) * VROW + 16 * (tr_G & 1) + 4 * (tr_i & 3);
 
-  auto tile_src = [&](int j, const uint16_t*& kb, const uint16_t*& vb, int64_t& kss, int64_t& vss, int& valid) {
-    if (j < n_rt) {
-      kb = kr + (int64_t)j * BN * krv.ss;
-      vb = vr + (int64_t)j * BN * vrv.ss;
-      kss = krv.ss;
-      vss = vrv.ss;
-      valid = min(BN, p.n_ref - j * BN);
-    } else {
-      const int jj = j - n_rt;
-      kb = ky + (int64_t)jj * BN * p.k_tgt.ss;
-      vb = vy + (int64_t)jj * BN * p.v_tgt.ss;
-      kss = p.k_tgt.ss;
-      vss = p.v_tgt.ss;
-      valid = min(BN, p.n_tgt - jj * BN);
+  // ---- prologue: K_0, K_1 and V_0 into LDS; S_0
+  Staging<D> stk, stv;
+  load_k(stk, 0);
+  load_v(stv, 0);
+  stage_store<D, true>(stk, kbuf[0], k_st);
+  stage_store<D, false>(stv, vbuf[0], v_st);
+  if (nt > 1) {
+    load_k(stk, 1);
+    stage_store<D, true>(stk, kbuf[1], k_st);
+  }
+  __syncthreads();
+  f32x16 sa[2], sb[2];
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    sa[mb] = f32x16{};
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbuf[0] + k_lane + 32 * mb * KROW + 16 * kk);
+      sa[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sa[mb], 0, 0, 0);
     }
-  };
+  }
+  __syncthreads();  // every wavefront has read K_0 before iteration 0 refills its buffer
 
   f32x16 o[DB];
 #pragma unroll
@@ -184,106 +258,134 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   float m_ref = -__builtin_inff(), l_ref = 0.f;
   const float c = p.sc_log2;
 
-  Prefetch<D> pf;
-  {
-    const uint16_t *kb, *vb;
-    int64_t kss, vss;
-    int valid;
-    tile_src(0, kb, vb, kss, vss, valid);
-    load_tile<D>(pf, kb, vb, kss, vss, valid, tid);
-    store_tile<D>(pf, lds[0], lds[0] + TILE, tid);
-  }
-  __syncthreads();
+  auto iteration = [&](int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
+    // Global loads for the tiles this iteration stages: K_{j+2} and V_{j+1}. Past the
+    // end the index is clamped to the last tile: the reload lands in a buffer that is
+    // never read again.
+    load_k(stk, min(j + 2, nt - 1));
+    load_v(stv, min(j + 1, nt - 1));
 
-  for (int j = 0; j < nt; ++j) {
-    int valid_next = 0;
-    if (j + 1 < nt) {
-      const uint16_t *kb, *vb;
-      int64_t kss, vss;
-      tile_src(j + 1, kb, vb, kss, vss, valid_next);
-      load_tile<D>(pf, kb, vb, kss, vss, valid_next, tid);
-    }
-    const uint16_t* ks = lds[j & 1];
-    const uint16_t* vts = ks + TILE;
-    const int valid = j < n_rt ? min(BN, p.n_ref - j * BN) : min(BN, p.n_tgt - (j - n_rt) * BN);
-
-    // ---- S^T = K Q^T for two 32-key blocks
-    f32x16 s[2];
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb) {
-      s[mb] = f32x16{};
-      const uint16_t* krow = ks + (32 * mb + sigma(n)) * D;
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const int phys = (2 * kk + g) ^ (n & 7);
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + phys * 8);
-        s[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], s[mb], 0, 0, 0);
-      }
-    }
+    const int valid = tile_valid(j);
     if (valid < BN) {  // ragged last tile of a segment: drop keys past its end
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = 32 * mb + 16 * (r >> 3) + 8 * g + (r & 7);
-          if (key >= valid) s[mb][r] = -__builtin_inff();
+          if (key >= valid) s_cur[mb][r] = -__builtin_inff();
         }
     }
 
-    // ---- online softmax in the exp2 domain (scores scaled by scale*log2(e))
-    float mx = -__builtin_inff();
+    // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by a slice
+    // of the softmax of S_j: the row max, then the probabilities of P blocks 0 and 1.
+    // At the last iteration the K buffer holds no tile and S_{j+1} is discarded.
+    const uint16_t* kb = kbuf[(j + 1) & 1];
+    auto k_operand = [&](int i) {  // i = KS * mb + kk
+      return *reinterpret_cast<const bf16x8*>(kb + k_lane + 32 * (i / KS) * KROW + 16 * (i % KS));
+    };
+    uint32_t pw[4][4];  // packed bf16 probabilities: P block s2, keys 16*s2 + 8*g + 2w, +1
+    float rs0 = 0.f, rs1 = 0.f, mx0 = 0.f, m_new = m_run;
+    auto prob_pair = [&](int q) {  // scores 2q, 2q+1 -> P block q/4, word q%4
+      const int mb = q >> 3, o2 = (2 * q) & 15;
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m_new));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2 + 1], c, -m_new));
+      rs0 += e0;
+      rs1 += e1;
+      bf16x2 pr;
+      pr[0] = (__bf16)e0;
+      pr[1] = (__bf16)e1;
+      uint32_t w = __builtin_bit_cast(uint32_t, pr);
+      pin(w);
+      pin(rs0);
+      pin(rs1);
+      pw[q >> 2][q & 3] = w;
+    };
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int mb = 0; mb < 2; ++mb) s_next[mb] = f32x16{};
+    bf16x8 ka[4];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[mb][r]);
-    mx = wave_xor32_max(mx);
-    const float m_new = fmaxf(m_run, mx * c);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    float rs = 0.f;
+    for (int i = 0; i < 4; ++i) ka[i] = k_operand(i);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int i = 0; i < NQK; ++i) {
+      s_next[i / KS] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i & 3], qreg[i % KS], s_next[i / KS], 0, 0, 0);
+      if (i + 4 < NQK) ka[i & 3] = k_operand(i + 4);
+      if (i == 0) {
+        float m = s_cur[0][0];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[mb][r], c, -m_new));
-        s[mb][r] = e;
-        rs += e;
+        for (int r = 1; r < 16; ++r) m = fmaxf(m, s_cur[0][r]);
+        mx0 = m;
+      } else if (i == 1) {
+        float m = mx0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s_cur[1][r]);
+        m = xor32_max(m) * c;
+        m_new = m > m_run + TAU ? m : m_run;  // lazy: move only on a large increase
+        pin(m_new);
+      } else if (i - 2 < 8) {
+        prob_pair(i - 2);  // pairs 0..7 fill P blocks 0 and 1
       }
-    rs = wave_xor32_add(rs);
-    l_run = l_run * alpha + rs;
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (NQK < 10) {  // head_dim 64: fewer MFMAs than softmax slices
+#pragma unroll
+      for (int q = NQK - 2; q < 8; ++q) prob_pair(q);
+    }
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 1 unless the max moved
     m_run = m_new;
     if (__any(alpha != 1.f)) {
+      l_run *= alpha;
 #pragma unroll
       for (int i = 0; i < DB; ++i) o[i] *= alpha;
     }
 
-    // ---- P^T to bf16 B operands: k-step s2 covers keys 16*s2 .. 16*s2+15
-    bf16x8 pb[4];
+    // ---- phase B: O^T += V_j^T P_j^T, P block-major; the probabilities of P blocks
+    // 2 and 3 are formed under the MFMAs of blocks 0 and 1. V^T operands come from
+    // LDS transpose reads issued two MFMAs ahead.
+    const uint16_t* vs = vbuf[j & 1];
+    auto v_operand = [&](int i) {  // i = DB * s2 + db
+      const uint16_t* a = vs + v_lane + 16 * (i / DB) * VROW + 32 * (i % DB);
+      const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(a));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(a + 4 * VROW));
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
+    bf16x8 va[3];
+    va[0] = v_operand(0);
+    va[1] = v_operand(1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int s2 = 0; s2 < 4; ++s2)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) pb[s2][i] = (__bf16)s[s2 >> 1][8 * (s2 & 1) + i];
-
-    // ---- O^T += V^T P^T
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const int d = 32 * db + n;
-      const int swz = (d ^ (d >> 3)) & 7;
-      const uint16_t* vrow = vts + d * BN;
-#pragma unroll
-      for (int s2 = 0; s2 < 4; ++s2) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(vrow + (((2 * s2 + g) ^ swz) * 8));
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[s2], o[db], 0, 0, 0);
+    for (int i = 0; i < NPV; ++i) {
+      const int s2 = i / DB;
+      const u32x4 pwv = {pw[s2][0], pw[s2][1], pw[s2][2], pw[s2][3]};
+      o[i % DB] =
+          __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], __builtin_bit_cast(bf16x8, pwv), o[i % DB], 0, 0, 0);
+      if (i + 2 < NPV) va[(i + 2) % 3] = v_operand(i + 2);
+      // pairs 8..15 fill P blocks 2 and 3 before the first MFMA that reads them
+      if (DB == 4 && i < 8) prob_pair(8 + i);
+      if (DB == 2 && i < 4) {
+        prob_pair(8 + 2 * i);
+        prob_pair(9 + 2 * i);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
+    l_run += xor32_add(rs0 + rs1);
 
     if (j == n_rt - 1) {  // end of the reference segment: freeze its statistics
       m_ref = m_run;
       l_ref = l_run;
       l_run = 0.f;
     }
-    if (j + 1 < nt) store_tile<D>(pf, lds[(j + 1) & 1], lds[(j + 1) & 1] + TILE, tid);
+    stage_store<D, true>(stk, kbuf[j & 1], k_st);
+    stage_store<D, false>(stv, vbuf[(j + 1) & 1], v_st);
     __syncthreads();
+  };
+
+  int j = 0;
+  for (; j + 1 < nt; j += 2) {
+    iteration(j, sa, sb);
+    iteration(j + 1, sb, sa);
   }
+  if (j < nt) iteration(j, sa, sb);
 
   // ---- epilogue
   const float L_R = l_ref > 0.f ? l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) : 0.f;

@@ -37,6 +37,9 @@ def compile_flags():
         "-Wall",
         "-Wno-unused-function",
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # MFMA accumulators in ordinary vector registers: the softmax reads the
+        # score tiles directly instead of copying them out of AGPRs every tile.
+        "-mllvm", "-amdgpu-mfma-vgpr-form",
         "-I", os.path.join(ROOT, "include"),
     ]
 

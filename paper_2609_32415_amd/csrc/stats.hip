@@ -129,11 +129,35 @@ __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t 
     s_react = st->reactivated;
   }
 
-  // Mean over target queries of the lagged per-query reference mass, one wavefront per (b, h).
+  // Mean over target queries of the lagged per-query reference mass, one wavefront per
+  // (b, h): 16-byte loads, four in flight per lane, then a fixed-order butterfly.
   for (int bh = wave; bh < BH; bh += GATE_THREADS / 64) {
     const float* row = mass_prev + (int64_t)bh * n_tgt;
     float s = 0.f;
-    for (int i = lane; i < n_tgt; i += 64) s += row[i];
+    int i0 = 0;
+    if ((reinterpret_cast<uintptr_t>(row) & 15) == 0) {
+      const int n4 = n_tgt >> 2;
+      const float4* r4 = reinterpret_cast<const float4*>(row);
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      int k = lane;
+      for (; k + 192 < n4; k += 256) {
+        const float4 a = r4[k], b2 = r4[k + 64], c2 = r4[k + 128], d2 = r4[k + 192];
+        acc.x += (a.x + b2.x) + (c2.x + d2.x);
+        acc.y += (a.y + b2.y) + (c2.y + d2.y);
+        acc.z += (a.z + b2.z) + (c2.z + d2.z);
+        acc.w += (a.w + b2.w) + (c2.w + d2.w);
+      }
+      for (; k < n4; k += 64) {
+        const float4 a = r4[k];
+        acc.x += a.x;
+        acc.y += a.y;
+        acc.z += a.z;
+        acc.w += a.w;
+      }
+      s = (acc.x + acc.y) + (acc.z + acc.w);
+      i0 = n4 << 2;
+    }
+    for (int i = i0 + lane; i < n_tgt; i += 64) s += row[i];
     s = wave_sum(s);
     if (lane == 0) m_head[bh] = s / (float)n_tgt;
   }
