@@ -275,7 +275,7 @@ def main():
     if args.sweep:
         from paper_2609_32415_amd.controller import run_sweep
 
-        out["sweep"] = run_sweep(device=dev)
+        out["sweep"] = run_sweep(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
     print(json.dumps(out), flush=True)
 
 

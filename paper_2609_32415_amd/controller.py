@@ -1,0 +1,179 @@
+"""Alg. 1 (monotone depth-adaptive reference reuse) over the library's kernels.
+
+Per denoising step and block the executor enqueues, on the current stream and
+without any host synchronisation:
+
+  refadapt_q_change    D of this block's target Q against the recorded one
+  refadapt_gate        head-mean D*M against theta_b, decision written on the device
+                       (block 0 also does the step bookkeeping: step 0 and the
+                       bounded-age refresh make every block of the step compute)
+  refadapt_joint_attn  RA_KV_DEVICE: REUSE -> target queries over the cached
+                       reference K/V; REACTIVATE -> all queries over the cache;
+                       COMPUTE -> all queries over fresh K/V
+  refadapt_cache_commit  fresh reference K/V -> cache and a_b <- t on COMPUTE
+
+and records the block's target Q (by reference) and the per-query reference
+mass of the attention it executed (ping-pong buffers) for the next step. The
+decisions stay on the device until the caller reads them.
+
+The block inputs are exogenous here: the caller supplies each block's fresh
+Q/K/V per step (the diffusion transformer whose hidden states would produce
+them is outside this library).
+
+``run_sweep`` runs the controller sweep: 60 blocks x 8 steps at the
+single-reference shapes, 3 x 3 threshold cells, against a full-fresh
+trajectory through the same harness.
+"""
+
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import ops, synth
+from .ops import COMPUTE, REACTIVATE, REUSE
+
+
+class Controller:
+    """Device-resident controller state and per-block buffers of one trajectory."""
+
+    def __init__(self, n_blocks, n_steps, batch, heads, n_ref, n_tgt, head_dim, theta, delta_max=None,
+                 mode="product", theta_m=None, dtype=torch.bfloat16, device="cuda:0", eps=1e-8):
+        self.nb, self.n_steps = n_blocks, n_steps
+        self.shape_r = (batch, heads, n_ref, head_dim)
+        self.shape_t = (batch, heads, n_tgt, head_dim)
+        self.mode, self.eps, self.device = mode, eps, device
+        tq = torch.as_tensor(theta, dtype=torch.float64).reshape(-1).expand(n_blocks)
+        if mode == "and":  # (theta_q, theta_m) pairs per block
+            tm = torch.as_tensor(theta_m, dtype=torch.float64).reshape(-1).expand(n_blocks)
+            th = torch.stack([tq, tm], 1).reshape(-1)
+        else:
+            th = tq
+        self.theta = th.to(torch.float32).contiguous().to(device)
+        self.state = ops.new_gate_state(device, delta_max or 0)
+        self.k_cache = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
+        self.v_cache = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
+        self.mass = [[torch.zeros((batch, heads, n_tgt), dtype=torch.float32, device=device) for _ in range(2)]
+                     for _ in range(n_blocks)]
+        self.parity = [0] * n_blocks
+        self.q_prev = [None] * n_blocks
+        self.age = torch.zeros(n_blocks, dtype=torch.int32, device=device)
+        self.d = torch.zeros((n_blocks, batch, heads), dtype=torch.float32, device=device)
+        self.decisions = torch.full((n_steps, n_blocks), -1, dtype=torch.int32, device=device)
+        self.scores = torch.zeros((n_steps, n_blocks, 3), dtype=torch.float32, device=device)
+        self.o_tgt = [torch.empty(self.shape_t, dtype=dtype, device=device) for _ in range(n_blocks)]
+        self.o_ref = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
+        self.ws = ops.q_change_workspace(torch.empty(self.shape_t, dtype=dtype, device=device))
+
+    def block(self, t, b, x):
+        """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``."""
+        q_prev = self.q_prev[b] if self.q_prev[b] is not None else x["q_tgt"]
+        ops.q_change(x["q_tgt"], q_prev, self.eps, out=self.d[b], workspace=self.ws)
+        dec = self.decisions[t, b:b + 1]
+        ops.gate(self.d[b], self.mass[b][self.parity[b]], self.theta, self.state, b, t, self.mode,
+                 decision_out=dec, score_out=self.scores[t, b])
+        nxt = 1 - self.parity[b]
+        ops.joint_attn(
+            x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"], v_ref=x["v_ref"],
+            k_cache=self.k_cache[b], v_cache=self.v_cache[b], kvsrc="device", decision=dec,
+            o_tgt=self.o_tgt[b], o_ref=self.o_ref[b], ref_mass=self.mass[b][nxt],
+        )
+        ops.cache_commit(x["k_ref"], x["v_ref"], self.k_cache[b], self.v_cache[b], decision=dec,
+                         age=self.age[b:b + 1], step=t)
+        self.q_prev[b] = x["q_tgt"]
+        self.parity[b] = nxt
+
+    def step(self, t, inputs):
+        """All blocks of step ``t``; ``inputs[b]`` is block b's dict of fresh tensors."""
+        for b in range(self.nb):
+            self.block(t, b, inputs[b])
+
+    def recorded_mass(self, b):
+        """Per-query reference mass of block b's most recently executed attention."""
+        return self.mass[b][self.parity[b]]
+
+
+def _sweep_inputs(w, device):
+    trajs = [synth.DeviceTrajectory(w, b, device, ref_sigma=(lambda t, b=b: synth.sweep_ref_drift(b, w.n_blocks)),
+                                    tgt_sigma=(lambda t: synth.sweep_tgt_drift(t, w.n_steps)))
+             for b in range(w.n_blocks)]
+    return trajs
+
+
+def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=None):
+    """One trajectory; returns (controller, per-step attention-path milliseconds)."""
+    ctl = Controller(w.n_blocks, w.n_steps, w.batch, w.heads, w.n_ref, w.n_tgt, w.head_dim, theta,
+                     delta_max=delta_max, mode=mode, theta_m=theta_m, device=device)
+    trajs = _sweep_inputs(w, device)
+    step_ms = []
+    for t in range(w.n_steps):
+        xs = [tr.step_tensors(t) for tr in trajs]
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        ctl.step(t, xs)
+        e1.record()
+        if keep is not None:
+            keep(t, ctl, xs)
+        torch.cuda.synchronize()
+        step_ms.append(e0.elapsed_time(e1))
+    return ctl, step_ms
+
+
+def run_sweep(device="cuda:0", w=None, log=None):
+    """The controller sweep (60 blocks x 8 steps, single-reference shapes).
+
+    For each (theta_q, theta_m) cell the product gate runs with
+    theta = theta_q * theta_m (one threshold on the head-mean D*M score). Reports
+    the reuse fraction over steps >= 1, the attention-path time (Q-change, gate,
+    attention and commit kernels of every block) against a full-fresh trajectory
+    through the same harness (bounded-age refresh every step), and the relative
+    change of the executed target output against full-fresh attention.
+    """
+    w = w or synth.workload("sweep")
+    base, base_ms = _timed_run(w, device, 0.0, delta_max=1)
+    full_ms = sum(base_ms)
+    if log:
+        log(f"sweep: full-fresh trajectory {full_ms:.1f} ms")
+    cells = []
+    for tq in w.theta_q:
+        for tm in w.theta_m:
+            theta = tq * tm
+            ctl, ms = _timed_run(w, device, theta, delta_max=None)
+            dec = ctl.decisions.cpu()
+            after0 = dec[1:]
+            errs = []
+
+            def keep(t, c, xs):  # untimed: relative change of executed vs full-fresh target output
+                for b in range(w.n_blocks):
+                    x = xs[b]
+                    fresh = ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_ref=x["k_ref"], v_ref=x["v_ref"],
+                                           ref_mass=False).o_tgt.float()
+                    diff = (c.o_tgt[b].float() - fresh).flatten(2).norm(dim=-1)
+                    errs.append((diff / (fresh.flatten(2).norm(dim=-1) + 1e-8)).flatten())
+
+            _timed_run(w, device, theta, delta_max=None, keep=keep)
+            e = torch.cat(errs).cpu()
+            cells.append({
+                "theta_q": tq, "theta_m": tm, "theta": theta,
+                "reuse_fraction": round(float((after0 == REUSE).float().mean()), 4),
+                "reuse_or_reactivate_fraction": round(float((after0 != COMPUTE).float().mean()), 4),
+                "attn_path_ms": round(sum(ms), 3),
+                "speedup_vs_full_fresh": round(full_ms / sum(ms), 3),
+                "boundary_block_per_step": [next((i for i, x in enumerate(row) if x == REACTIVATE), None)
+                                            for row in dec.tolist()],
+                "impact_mean": round(float(e.mean()), 5),
+                "impact_p99": round(float(e.quantile(0.99)), 5),
+                "impact_max": round(float(e.max()), 5),
+            })
+            if log:
+                log(f"sweep: cell theta_q={tq} theta_m={tm}: {cells[-1]['attn_path_ms']} ms, "
+                    f"speedup {cells[-1]['speedup_vs_full_fresh']}, reuse {cells[-1]['reuse_fraction']}")
+    return {
+        "workload": f"{w.n_blocks} blocks x {w.n_steps} steps, batch {w.batch}, {w.heads} heads, head_dim "
+                    f"{w.head_dim}, n_ref {w.n_ref}, n_tgt {w.n_tgt}",
+        "full_fresh_attn_path_ms": round(full_ms, 3),
+        "max_speedup_bound": round(w.n_steps / (1 + (w.n_steps - 1) * w.n_tgt / (w.n_ref + w.n_tgt)), 3),
+        "cells": cells,
+    }

@@ -236,3 +236,56 @@ def sample_rows(n, count, seed, include_edges=True):
     if include_edges and n > 0:
         idx.update({0, n - 1})
     return np.array(sorted(idx), dtype=np.int64)
+
+
+class DeviceTrajectory:
+    """The same recipe as ``Trajectory`` drawn on a GPU with torch's generator.
+
+    Used where host generation would be too slow (the 60-block sweep holds
+    about 9 GB of base tensors): base Q/K/V ~ N(0, 1), the key-bias
+    construction, then a random walk with per-step sigmas. Values are rounded
+    to the run dtype. Seeded per (workload seed, block); not bit-identical to
+    the numpy generator.
+    """
+
+    def __init__(self, w, block, device, ref_sigma=None, tgt_sigma=None):
+        import torch
+
+        self.torch = torch
+        self.w, self.block, self.device = w, block, device
+        self.ref_sigma = ref_sigma if ref_sigma is not None else (lambda t: w.ref_drift)
+        self.tgt_sigma = tgt_sigma if tgt_sigma is not None else (lambda t: w.tgt_drift)
+        self.gen = torch.Generator(device=device)
+        self.gen.manual_seed(int(w.seed) * 1_000_003 + int(block))
+        self._state = None
+        self._t = -1
+
+    def _randn(self, n):
+        w = self.w
+        return self.torch.randn((w.batch, w.heads, n, w.head_dim), generator=self.gen, device=self.device)
+
+    def step_tensors(self, t):
+        torch, w = self.torch, self.w
+        if t != self._t + 1:
+            raise ValueError("steps must be visited in order")
+        if t == 0:
+            st = {r: self._randn(w.n_ref if r.endswith("_ref") else w.n_tgt) for r in ROLES}
+            if w.key_bias:
+                u = torch.randn((w.batch, w.heads, w.head_dim), generator=self.gen, device=self.device)
+                u = u / u.norm(dim=-1, keepdim=True)
+                st["k_ref"] += 0.5 * math.sqrt(w.head_dim) * u[:, :, None, :]
+                shared = torch.rand((w.batch, w.heads, w.n_tgt), generator=self.gen, device=self.device) < 0.3
+                lam = torch.tensor([_lambda(w, self.block, h) for h in range(w.heads)], device=self.device)
+                comp = torch.where(shared, torch.ones_like(shared, dtype=torch.float32), -lam[None, :, None])
+                cur = torch.einsum("bhnd,bhd->bhn", st["q_tgt"], u)
+                st["q_tgt"] += (comp - cur)[..., None] * u[:, :, None, :]
+            self._state = st
+        else:
+            for role in ROLES:
+                sig = self.ref_sigma(t) if role.endswith("_ref") else self.tgt_sigma(t)
+                if sig:
+                    n = w.n_ref if role.endswith("_ref") else w.n_tgt
+                    self._state[role].add_(self._randn(n), alpha=sig)
+        self._t = t
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        return {k: v.to(dt) for k, v in self._state.items()}
