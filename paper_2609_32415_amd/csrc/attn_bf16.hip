@@ -17,8 +17,14 @@
 // of O += V_j^T P_j^T, under the first half of which the probabilities of the
 // second half of P_j are formed (phase B). sched_barrier fences keep that
 // order, so the vector ALU works while the matrix core runs. K tiles run one
-// tile ahead of V tiles through two LDS buffers each, refilled from registers
-// loaded at the top of the iteration; one barrier per tile.
+// tile ahead of V tiles through two LDS buffers each, refilled from registers:
+// the next K tile is loaded at the top of the iteration, the next V tile at the
+// start of phase B, and both are stored after phase B; one barrier per tile.
+//
+// Two workgroups share a CU (two wavefronts per SIMD, at most 256 vector
+// registers per lane each): while one wavefront forms probabilities the other
+// keeps the matrix core busy. Staging V only over phase B keeps the register
+// peak of phase A under that limit.
 //
 // Online softmax in the exp2 domain with lazy rescaling: a lane moves its
 // running max only when a tile's max exceeds it by more than 2^8, so the O
@@ -133,7 +139,7 @@ __device__ __forceinline__ void stage_store(const Staging<D>& st, uint16_t* tile
 }
 
 template <int D>
-__global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
+__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // MFMA k-steps over the head dim for S^T
   constexpr int DB = D / 32;   // 32-row blocks of the O^T accumulator
   constexpr int NQK = 2 * KS;  // MFMAs of one S^T tile
@@ -215,10 +221,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     const uint16_t* qp = static_cast<const uint16_t*>(qv.p) + b * qv.sb + h * qv.sh + (int64_t)qrow * qv.ss;
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      u32x4 raw = qvalid ? *reinterpret_cast<const u32x4*>(qp + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
-      // Q^T is only ever an MFMA operand: keep it in accumulation registers, which
-      // leaves the vector registers to the two score tiles and the softmax.
-      asm volatile("" : "+a"(raw));
+      const u32x4 raw = qvalid ? *reinterpret_cast<const u32x4*>(qp + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
       qreg[kk] = __builtin_bit_cast(bf16x8, raw);
     }
   }
@@ -259,11 +262,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const float c = p.sc_log2;
 
   auto iteration = [&](int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
-    // Global loads for the tiles this iteration stages: K_{j+2} and V_{j+1}. Past the
-    // end the index is clamped to the last tile: the reload lands in a buffer that is
-    // never read again.
+    // Global loads for the tiles this iteration stages: K_{j+2} here, V_{j+1} at the
+    // start of phase B. Past the end the index is clamped to the last tile: the
+    // reload lands in a buffer that is never read again.
     load_k(stk, min(j + 2, nt - 1));
-    load_v(stv, min(j + 1, nt - 1));
 
     const int valid = tile_valid(j);
     if (valid < BN) {  // ragged last tile of a segment: drop keys past its end
@@ -342,6 +344,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // ---- phase B: O^T += V_j^T P_j^T, P block-major; the probabilities of P blocks
     // 2 and 3 are formed under the MFMAs of blocks 0 and 1. V^T operands come from
     // LDS transpose reads issued two MFMAs ahead.
+    load_v(stv, min(j + 1, nt - 1));
     const uint16_t* vs = vbuf[j & 1];
     auto v_operand = [&](int i) {  // i = DB * s2 + db
       const uint16_t* a = vs + v_lane + 16 * (i / DB) * VROW + 32 * (i % DB);
