@@ -99,6 +99,8 @@ typedef struct {
   float* ref_mass;               /* out [B, H, n_tgt] contiguous fp32, or NULL */
   float* lse_tgt;                /* out [B, H, n_tgt, 2] = (lse_ref, lse_all), or NULL */
   float* ref_mass_refq;          /* out [B, H, n_ref] reference-query mass on reference keys, or NULL */
+  void* workspace;               /* device scratch for key-split partial results, or NULL (no split) */
+  size_t workspace_bytes;        /* its size; >= refadapt_joint_attn_workspace_size(desc) when non-NULL */
 } ra_attn_args;
 
 /*
@@ -118,18 +120,37 @@ typedef struct {
  * bf16 MFMA for RA_BF16). Writing ref_mass / lse does not change o (the
  * attention output is bit-identical with them on or off).
  *
- * Under RA_KV_DEVICE the grid covers all queries and reference-query
- * workgroups exit at once when *decision == RA_REUSE; o_ref is then left
- * untouched.
+ * Under RA_KV_DEVICE the launch is sized for every query and the workgroups
+ * read *decision first: on RA_REUSE only target query rows are computed and
+ * o_ref is left untouched.
+ *
+ * Load balance (bf16): with a workspace, query tiles of a last, partly filled
+ * round of workgroups are split into key-tile ranges whose partial softmax
+ * statistics a second kernel merges (the same rescale-and-add the online
+ * softmax applies across key tiles). Results then differ from the unsplit
+ * launch only by fp32 rounding; a given desc on a given device always takes
+ * the same split, so repeated calls are bitwise identical. With
+ * workspace == NULL nothing is split. The workspace needs no initialisation,
+ * must be 16-byte aligned and must not be used by another call that runs
+ * concurrently. The fp32 path never splits.
  *
  * Errors: RA_EINVAL for a null desc/args, sizes out of range, unknown enums,
  * or a required pointer that is NULL (q/k/v/o_tgt always; k_ref/v_ref when
  * fresh K/V may be read and n_ref > 0; k_cache/v_cache when cached K/V may be
  * read and n_ref > 0; q_ref/o_ref when reference queries may attend and
  * n_ref > 0; decision under RA_KV_DEVICE). RA_EUNSUPPORTED for head_dim not
- * in {64, 128} or misaligned tensors.
+ * in {64, 128} or misaligned tensors or workspace. RA_EWORKSPACE for a
+ * non-NULL workspace smaller than refadapt_joint_attn_workspace_size(desc).
  */
 ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream);
+
+/*
+ * refadapt_joint_attn_workspace_size - bytes of workspace that let
+ * refadapt_joint_attn split key ranges for `desc` on the CURRENT device (the
+ * split depends on the device's compute-unit count). 0 when no split pays or
+ * for an invalid desc (refadapt_joint_attn then reports the error).
+ */
+size_t refadapt_joint_attn_workspace_size(const ra_attn_desc* desc);
 
 /*
  * refadapt_q_change - consecutive relative change of the target queries.

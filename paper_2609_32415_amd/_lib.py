@@ -34,6 +34,7 @@ RA_GATE_PRODUCT, RA_GATE_Q_ONLY, RA_GATE_MASS_ONLY, RA_GATE_AND = 0, 1, 2, 3
 
 EXPORTED = (
     "refadapt_joint_attn",
+    "refadapt_joint_attn_workspace_size",
     "refadapt_q_change_workspace_size",
     "refadapt_q_change",
     "refadapt_gate",
@@ -82,6 +83,8 @@ class ra_attn_args(ctypes.Structure):
         ("ref_mass", ctypes.c_void_p),
         ("lse_tgt", ctypes.c_void_p),
         ("ref_mass_refq", ctypes.c_void_p),
+        ("workspace", ctypes.c_void_p),
+        ("workspace_bytes", ctypes.c_size_t),
     ]
 
 
@@ -110,6 +113,8 @@ def _load():
     i32, vp, f32 = ctypes.c_int32, ctypes.c_void_p, ctypes.c_float
     lib.refadapt_joint_attn.argtypes = [ctypes.POINTER(ra_attn_desc), ctypes.POINTER(ra_attn_args), vp]
     lib.refadapt_joint_attn.restype = i32
+    lib.refadapt_joint_attn_workspace_size.argtypes = [ctypes.POINTER(ra_attn_desc)]
+    lib.refadapt_joint_attn_workspace_size.restype = ctypes.c_size_t
     lib.refadapt_q_change_workspace_size.argtypes = [i32, i32, i32, i32]
     lib.refadapt_q_change_workspace_size.restype = ctypes.c_size_t
     lib.refadapt_q_change.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, vp, vp, ctypes.c_size_t, vp]
@@ -137,6 +142,10 @@ def _check(status):
 def refadapt_joint_attn(desc, args, stream):
     """Forward to ``refadapt_joint_attn``; raises RefadaptError on a non-OK status."""
     return _check(LIB.refadapt_joint_attn(ctypes.byref(desc), ctypes.byref(args), stream))
+
+
+def refadapt_joint_attn_workspace_size(desc):
+    return int(LIB.refadapt_joint_attn_workspace_size(ctypes.byref(desc)))
 
 
 def refadapt_q_change_workspace_size(batch, heads, n_tgt, head_dim):

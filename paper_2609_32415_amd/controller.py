@@ -64,7 +64,9 @@ class Controller:
         self.scores = torch.zeros((n_steps, n_blocks, 3), dtype=torch.float32, device=device)
         self.o_tgt = [torch.empty(self.shape_t, dtype=dtype, device=device) for _ in range(n_blocks)]
         self.o_ref = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
-        self.ws = ops.q_change_workspace(torch.empty(self.shape_t, dtype=dtype, device=device))
+        q_like = torch.empty(self.shape_t, dtype=dtype, device=device)
+        self.ws = ops.q_change_workspace(q_like)
+        self.attn_ws = ops.attn_workspace(q_like, n_ref, kvsrc="device")
 
     def block(self, t, b, x):
         """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``."""
@@ -77,7 +79,7 @@ class Controller:
         ops.joint_attn(
             x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"], v_ref=x["v_ref"],
             k_cache=self.k_cache[b], v_cache=self.v_cache[b], kvsrc="device", decision=dec,
-            o_tgt=self.o_tgt[b], o_ref=self.o_ref[b], ref_mass=self.mass[b][nxt],
+            o_tgt=self.o_tgt[b], o_ref=self.o_ref[b], ref_mass=self.mass[b][nxt], workspace=self.attn_ws,
         )
         ops.cache_commit(x["k_ref"], x["v_ref"], self.k_cache[b], self.v_cache[b], decision=dec,
                          age=self.age[b:b + 1], step=t)

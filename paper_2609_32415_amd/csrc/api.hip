@@ -7,9 +7,10 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <algorithm>
 #include <string>
 
-#include "../../include/refadapt.h"
+#include "refadapt.h"
 #include "internal.h"
 
 using namespace refadapt;
@@ -54,6 +55,108 @@ ra_status check_tensor(const char* name, const ra_tensor& t, int dtype, int32_t 
   return RA_OK;
 }
 
+// ---- work decomposition of the bf16 attention launch
+//
+// All query tiles of a launch cost the same (each attends to every key tile),
+// so the resident workgroups (slots = CUs x workgroups per CU) run them in
+// rounds. Cost model in units of "one key tile processed by every resident
+// workgroup": a round of items of L key tiles costs L, or kLoneRound * L when
+// the round holds no more items than there are CUs (a workgroup alone on its
+// CU runs faster); a chunk adds a fixed start-up and drain of kChunkOverhead
+// key tiles; the merge costs its partial-result traffic. The plan keeps the
+// largest number of whole rounds and splits only the remainder (plus, when it
+// pays, one more round) into chunks of at least kMinChunk key tiles.
+constexpr int kMinChunk = 4;
+constexpr double kChunkOverhead = 2.0;
+constexpr double kLoneRound = 0.67;
+constexpr int kMaxChunks = 32;
+
+SplitPlan whole_plan(int64_t tiles) {
+  return SplitPlan{(int32_t)tiles, 0, 1, (int32_t)tiles};
+}
+
+// Cost of running `items` items of `len` key tiles each in rounds of `slots`.
+double rounds_cost(int64_t items, double len, int64_t slots, int64_t cus) {
+  const int64_t full = items / slots, last = items - full * slots;
+  return full * len + (last == 0 ? 0.0 : last > cus ? len : kLoneRound * len);
+}
+
+SplitPlan plan_split(int64_t tiles, int nt, AttnSlots sl, int head_dim) {
+  SplitPlan best = whole_plan(tiles);
+  const int64_t slots = (int64_t)sl.cus * sl.per_cu;
+  if (tiles <= 0 || slots <= 0 || nt < 2 * kMinChunk) return best;
+  // A split must beat whole tiles by 3%; among splits the cheapest wins.
+  double best_cost = 0.97 * rounds_cost(tiles, nt, slots, sl.cus);
+  // Seconds for every resident workgroup to process one key tile (~1 PFLOP/s of
+  // attention) and to move one split item's partial rows twice (~4 TB/s).
+  const double tile_s = slots * 4.0 * kAttnBf16BM * kAttnBf16BN * head_dim / 1.0e15;
+  const double item_s = 2.0 * kAttnBf16BM * (head_dim + 4) * 4.0 / 4.0e12;
+  for (int extra = 0; extra < 2; ++extra) {
+    const int64_t rem = tiles % slots + (int64_t)extra * slots;
+    if (rem == 0 || rem > tiles) continue;
+    const int64_t rounds = (tiles - rem) / slots;
+    for (int c = 2; c <= kMaxChunks && c * kMinChunk <= nt; ++c) {
+      const int64_t items = rem * c;
+      if (items > 2 * slots) break;
+      const int chunk = (nt + c - 1) / c;
+      const double cost = (double)rounds * nt + rounds_cost(items, chunk + kChunkOverhead, slots, sl.cus) +
+                          (items * item_s + 5e-6) / tile_s;
+      if (cost < best_cost) {
+        best_cost = cost;
+        best = SplitPlan{(int32_t)(tiles - rem), (int32_t)rem, c, (int32_t)(tiles - rem + items)};
+      }
+    }
+  }
+  return best;
+}
+
+// Plans of one bf16 launch (plan[0]: the launch's query set, plan[1]: target
+// query tiles only) and the workspace bytes their split items need.
+struct LaunchPlan {
+  SplitPlan plan[2];
+  int64_t qt_ref, qt_tgt;
+  size_t ws_bytes;
+  size_t part_o_bytes;
+};
+
+LaunchPlan plan_launch(const ra_attn_desc& d, bool split) {
+  LaunchPlan lp{};
+  const bool device = d.kvsrc == RA_KV_DEVICE;
+  const bool ref_queries = (device || d.qset == RA_Q_ALL) && d.n_ref > 0;
+  const int bm = d.dtype == RA_BF16 ? kAttnBf16BM : kAttnF32BM;
+  lp.qt_ref = ref_queries ? (d.n_ref + bm - 1) / bm : 0;
+  lp.qt_tgt = (d.n_tgt + bm - 1) / bm;
+  const int64_t bh = (int64_t)d.batch * d.heads;
+  const int64_t all = bh * (lp.qt_ref + lp.qt_tgt), tgt = bh * lp.qt_tgt;
+  lp.plan[0] = whole_plan(all);
+  lp.plan[1] = device ? whole_plan(tgt) : lp.plan[0];
+  if (!split || d.dtype != RA_BF16 || all > 0x7fffffff) return lp;
+  const AttnSlots slots = attn_bf16_slots(d.head_dim);
+  const int nt = (d.n_ref + kAttnBf16BN - 1) / kAttnBf16BN + (d.n_tgt + kAttnBf16BN - 1) / kAttnBf16BN;
+  lp.plan[0] = plan_split(all, nt, slots, d.head_dim);
+  lp.plan[1] = device ? plan_split(tgt, nt, slots, d.head_dim) : lp.plan[0];
+  int64_t items = 0;
+  for (const SplitPlan& pl : lp.plan) items = std::max<int64_t>(items, (int64_t)pl.split_tiles * pl.chunks);
+  lp.part_o_bytes = (size_t)items * kAttnBf16BM * d.head_dim * sizeof(float);
+  lp.ws_bytes = items > 0 ? lp.part_o_bytes + (size_t)items * kAttnBf16BM * 4 * sizeof(float) : 0;
+  return lp;
+}
+
+ra_status check_attn_desc(const ra_attn_desc* desc, const char* who) {
+  if (!desc) return fail(RA_EINVAL, "%s: null desc", who);
+  const ra_attn_desc& d = *desc;
+  if (d.batch < 1 || d.heads < 1) return fail(RA_EINVAL, "%s: batch and heads must be >= 1", who);
+  if (d.n_tgt < 1) return fail(RA_EINVAL, "%s: n_tgt must be >= 1 (got %d)", who, d.n_tgt);
+  if (d.n_ref < 0) return fail(RA_EINVAL, "%s: n_ref must be >= 0 (got %d)", who, d.n_ref);
+  if (d.dtype != RA_BF16 && d.dtype != RA_F32) return fail(RA_EINVAL, "%s: unknown dtype %d", who, d.dtype);
+  if (d.qset != RA_Q_TARGET && d.qset != RA_Q_ALL) return fail(RA_EINVAL, "%s: unknown qset %d", who, d.qset);
+  if (d.kvsrc < RA_KV_FRESH || d.kvsrc > RA_KV_DEVICE) return fail(RA_EINVAL, "%s: unknown kvsrc %d", who, d.kvsrc);
+  if (d.head_dim != 64 && d.head_dim != 128)
+    return fail(RA_EUNSUPPORTED, "%s: head_dim %d not supported (64 or 128)", who, d.head_dim);
+  if (!std::isfinite(d.scale)) return fail(RA_EINVAL, "%s: scale must be finite", who);
+  return RA_OK;
+}
+
 ra_status launch_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(RA_ELAUNCH, "%s: %s", what, hipGetErrorString(e));
   return ok();
@@ -67,25 +170,21 @@ const char* refadapt_last_error(void) { return g_last_error.c_str(); }
 
 const char* refadapt_version(void) { return "refadapt 0.1 gfx950"; }
 
-ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream) {
-  if (!desc || !args) return fail(RA_EINVAL, "joint_attn: null desc or args");
-  const ra_attn_desc& d = *desc;
-  if (d.batch < 1 || d.heads < 1) return fail(RA_EINVAL, "joint_attn: batch and heads must be >= 1");
-  if (d.n_tgt < 1) return fail(RA_EINVAL, "joint_attn: n_tgt must be >= 1 (got %d)", d.n_tgt);
-  if (d.n_ref < 0) return fail(RA_EINVAL, "joint_attn: n_ref must be >= 0 (got %d)", d.n_ref);
-  if (d.dtype != RA_BF16 && d.dtype != RA_F32) return fail(RA_EINVAL, "joint_attn: unknown dtype %d", d.dtype);
-  if (d.qset != RA_Q_TARGET && d.qset != RA_Q_ALL) return fail(RA_EINVAL, "joint_attn: unknown qset %d", d.qset);
-  if (d.kvsrc < RA_KV_FRESH || d.kvsrc > RA_KV_DEVICE) return fail(RA_EINVAL, "joint_attn: unknown kvsrc %d", d.kvsrc);
-  if (d.head_dim != 64 && d.head_dim != 128)
-    return fail(RA_EUNSUPPORTED, "joint_attn: head_dim %d not supported (64 or 128)", d.head_dim);
-  if (!std::isfinite(d.scale)) return fail(RA_EINVAL, "joint_attn: scale must be finite");
+size_t refadapt_joint_attn_workspace_size(const ra_attn_desc* desc) {
+  if (check_attn_desc(desc, "joint_attn_workspace_size") != RA_OK) return 0;
+  return plan_launch(*desc, true).ws_bytes;
+}
 
+ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream) {
+  ra_status s;
+  if ((s = check_attn_desc(desc, "joint_attn")) != RA_OK) return s;
+  if (!args) return fail(RA_EINVAL, "joint_attn: null args");
+  const ra_attn_desc& d = *desc;
   const ra_attn_args& a = *args;
   const bool device = d.kvsrc == RA_KV_DEVICE;
   const bool ref_queries = (device || d.qset == RA_Q_ALL) && d.n_ref > 0;
   const bool reads_fresh = d.n_ref > 0 && (d.kvsrc == RA_KV_FRESH || device);
   const bool reads_cache = d.n_ref > 0 && (d.kvsrc == RA_KV_CACHE || device);
-  ra_status s;
   if ((s = check_tensor("q_tgt", a.q_tgt, d.dtype, d.n_tgt, d.head_dim)) != RA_OK) return s;
   if ((s = check_tensor("k_tgt", a.k_tgt, d.dtype, d.n_tgt, d.head_dim)) != RA_OK) return s;
   if ((s = check_tensor("v_tgt", a.v_tgt, d.dtype, d.n_tgt, d.head_dim)) != RA_OK) return s;
@@ -129,12 +228,22 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   const float scale = d.scale > 0.f ? d.scale : 1.0f / std::sqrt((float)d.head_dim);
   p.sc_log2 = scale * 1.4426950408889634f;
 
-  const int bm = d.dtype == RA_BF16 ? kAttnBf16BM : kAttnF32BM;
-  p.qt_ref = ref_queries ? (d.n_ref + bm - 1) / bm : 0;
-  p.qt_tgt = (d.n_tgt + bm - 1) / bm;
-  const int64_t total = (int64_t)d.batch * d.heads * (p.qt_ref + p.qt_tgt);
+  const LaunchPlan lp = plan_launch(d, a.workspace != nullptr);
+  const int64_t total = (int64_t)d.batch * d.heads * (lp.qt_ref + lp.qt_tgt);
   if (total > 0x7fffffff) return fail(RA_EUNSUPPORTED, "joint_attn: problem too large for one launch");
+  if (a.workspace != nullptr) {
+    if (a.workspace_bytes < lp.ws_bytes)
+      return fail(RA_EWORKSPACE, "joint_attn: workspace needs %zu bytes (got %zu)", lp.ws_bytes, a.workspace_bytes);
+    if ((reinterpret_cast<uintptr_t>(a.workspace) & 15) != 0)
+      return fail(RA_EUNSUPPORTED, "joint_attn: workspace must be 16-byte aligned");
+  }
+  p.qt_ref = (int32_t)lp.qt_ref;
+  p.qt_tgt = (int32_t)lp.qt_tgt;
   p.total_tiles = (int32_t)total;
+  p.plan[0] = lp.plan[0];
+  p.plan[1] = lp.plan[1];
+  p.part_o = static_cast<float*>(a.workspace);
+  p.part_st = lp.ws_bytes ? reinterpret_cast<float4*>(static_cast<char*>(a.workspace) + lp.part_o_bytes) : nullptr;
 
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const hipError_t e = d.dtype == RA_BF16 ? launch_attn_bf16(p, d.head_dim, st) : launch_attn_f32(p, d.head_dim, st);

@@ -1,6 +1,6 @@
 // Joint attention over [reference; target] keys on bf16 MFMA (gfx950).
 //
-// One workgroup = 4 wavefronts = 128 query rows of one (batch, head); each
+// One workgroup = 8 wavefronts = 256 query rows of one (batch, head); each
 // wavefront owns 32 query rows. Key/value tiles of 64 rows stream through LDS,
 // reference tiles first (from the fresh or the cached reference K/V, chosen
 // once per workgroup) and then target tiles.
@@ -21,10 +21,11 @@
 // the next K tile is loaded at the top of the iteration, the next V tile at the
 // start of phase B, and both are stored after phase B; one barrier per tile.
 //
-// Two workgroups share a CU (two wavefronts per SIMD, at most 256 vector
+// One workgroup fills a CU with two wavefronts per SIMD (at most 256 vector
 // registers per lane each): while one wavefront forms probabilities the other
-// keeps the matrix core busy. Staging V only over phase B keeps the register
-// peak of phase A under that limit.
+// keeps the matrix core busy, and the eight wavefronts share every K/V tile
+// staged in LDS (two 16-byte chunks per thread per tile). Staging V only over
+// phase B keeps the register peak of phase A under that limit.
 //
 // Online softmax in the exp2 domain with lazy rescaling: a lane moves its
 // running max only when a tile's max exceeds it by more than 2^8, so the O
@@ -38,8 +39,19 @@
 // L_R = l_R * 2^(m_R - m) and L_Y = l are the reference and target parts of
 // the softmax denominator in one scale; mass = L_R / (L_R + L_Y) lies in
 // [0, 1] by construction and equals exp(lse_R - lse_all).
+//
+// Load balance: all query tiles cost the same, so the launch runs in rounds of
+// as many workgroups as the device holds at once. When the last round would be
+// only partly full, the host plan cuts its query tiles into key-tile chunks
+// (more, shorter workgroups). A chunk keeps the same split statistics over its
+// key range and writes its unnormalised output with (m, l_Y, m_R, l_R) to a
+// workspace; attn_merge_kernel rescales the chunks to their common maximum and
+// sums them, which is the same reduction the online softmax performs across
+// key tiles.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <atomic>
 
 #include "internal.h"
 
@@ -55,8 +67,8 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 
 constexpr int BM = kAttnBf16BM;  // query rows per workgroup
-constexpr int BN = 64;           // keys per LDS tile
-constexpr int NT = 256;          // threads per workgroup
+constexpr int BN = kAttnBf16BN;  // keys per LDS tile
+constexpr int NT = 512;          // threads per workgroup
 constexpr float TAU = 8.0f;      // lazy-rescale threshold (log2 units)
 
 // Row permutation of a 32-key MFMA block: swaps bits 2 and 3 of the row index.
@@ -139,7 +151,7 @@ __device__ __forceinline__ void stage_store(const Staging<D>& st, uint16_t* tile
 }
 
 template <int D>
-__global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
+__global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // MFMA k-steps over the head dim for S^T
   constexpr int DB = D / 32;   // 32-row blocks of the O^T accumulator
   constexpr int NQK = 2 * KS;  // MFMAs of one S^T tile
@@ -152,21 +164,38 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const int lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, n = lane & 31;
 
-  // ---- which (batch, head, query tile) this workgroup owns
-  const int tile = xcd_remap(blockIdx.x, p.total_tiles);
-  const int qt_bh = p.qt_ref + p.qt_tgt;
+  // ---- which (batch, head, query tile) and which key tiles this workgroup owns
+  bool use_cache = p.kvsrc == KV_CACHE;
+  bool tgt_only = false;  // a reused block (KV_DEVICE): reference query rows are skipped
+  if (p.kvsrc == KV_DEVICE) {
+    const int dec = __builtin_amdgcn_readfirstlane(*p.decision);
+    use_cache = dec != DEC_COMPUTE;
+    tgt_only = dec == DEC_REUSE;
+  }
+  const SplitPlan pl = p.plan[tgt_only ? 1 : 0];
+  const int qt_ref = tgt_only ? 0 : p.qt_ref;
+  const int n_rt = (p.n_ref + BN - 1) / BN;
+  const int n_yt = (p.n_tgt + BN - 1) / BN;
+  const int nt = n_rt + n_yt;
+  const int w = blockIdx.x;
+  if (w >= pl.total_items) return;
+  int tile, j0 = 0, j1 = nt, slot = -1;
+  if (w < pl.whole) {
+    tile = xcd_remap(w, pl.whole);
+  } else {  // key chunk c of a split tile: key tiles [c * nt / chunks, (c + 1) * nt / chunks)
+    // The chunks of neighbouring tiles of one (batch, head) go to one XCD, as whole tiles do.
+    slot = xcd_remap(w - pl.whole, pl.total_items - pl.whole);
+    const int st = slot / pl.chunks, c = slot - st * pl.chunks;
+    tile = pl.whole + st;
+    j0 = c * nt / pl.chunks;
+    j1 = (c + 1) * nt / pl.chunks;
+  }
+  const int qt_bh = qt_ref + p.qt_tgt;
   const int bh = tile / qt_bh;
   int qt = tile - bh * qt_bh;
   const int b = bh / p.H, h = bh - b * p.H;
-  const bool ref_rows = qt < p.qt_ref;
-  if (!ref_rows) qt -= p.qt_ref;
-
-  bool use_cache = p.kvsrc == KV_CACHE;
-  if (p.kvsrc == KV_DEVICE) {
-    const int dec = *p.decision;
-    if (ref_rows && dec == DEC_REUSE) return;  // reference rows are skipped on a reused block
-    use_cache = dec != DEC_COMPUTE;
-  }
+  const bool ref_rows = qt < qt_ref;
+  if (!ref_rows) qt -= qt_ref;
 
   const View& qv = ref_rows ? p.q_ref : p.q_tgt;
   const View& ov = ref_rows ? p.o_ref : p.o_tgt;
@@ -178,9 +207,6 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const uint16_t* ky = static_cast<const uint16_t*>(p.k_tgt.p) + b * p.k_tgt.sb + h * p.k_tgt.sh;
   const uint16_t* vy = static_cast<const uint16_t*>(p.v_tgt.p) + b * p.v_tgt.sb + h * p.v_tgt.sh;
 
-  const int n_rt = (p.n_ref + BN - 1) / BN;
-  const int n_yt = (p.n_tgt + BN - 1) / BN;
-  const int nt = n_rt + n_yt;
   auto tile_valid = [&](int j) { return j < n_rt ? min(BN, p.n_ref - j * BN) : min(BN, p.n_tgt - (j - n_rt) * BN); };
   // Per-thread staging offsets (bytes into a tile, per segment) and LDS offsets.
   constexpr int KCH = Layout<D>::KCH;
@@ -231,14 +257,15 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const int tr_i = lane & 15, tr_G = lane >> 4;  // 16-lane group of the transpose read
   const int v_lane = (8 * (tr_G >> 1) + (tr_i >> 2)) * VROW + 16 * (tr_G & 1) + 4 * (tr_i & 3);
 
-  // ---- prologue: K_0, K_1 and V_0 into LDS; S_0
+  // ---- prologue: K_{j0}, K_{j0+1} and V_{j0} into LDS; S_{j0}. Tile j lives in
+  // buffer (j - j0) & 1.
   Staging<D> stk, stv;
-  load_k(stk, 0);
-  load_v(stv, 0);
+  load_k(stk, j0);
+  load_v(stv, j0);
   stage_store<D, true>(stk, kbuf[0], k_st);
   stage_store<D, false>(stv, vbuf[0], v_st);
-  if (nt > 1) {
-    load_k(stk, 1);
+  if (j0 + 1 < j1) {
+    load_k(stk, j0 + 1);
     stage_store<D, true>(stk, kbuf[1], k_st);
   }
   __syncthreads();
@@ -252,7 +279,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       sa[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sa[mb], 0, 0, 0);
     }
   }
-  __syncthreads();  // every wavefront has read K_0 before iteration 0 refills its buffer
+  __syncthreads();  // every wavefront has read K_{j0} before the first iteration refills its buffer
 
   f32x16 o[DB];
 #pragma unroll
@@ -262,10 +289,11 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   const float c = p.sc_log2;
 
   auto iteration = [&](int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
+    const int jb = (j - j0) & 1;  // LDS buffer of K_j and V_j
     // Global loads for the tiles this iteration stages: K_{j+2} here, V_{j+1} at the
-    // start of phase B. Past the end the index is clamped to the last tile: the
-    // reload lands in a buffer that is never read again.
-    load_k(stk, min(j + 2, nt - 1));
+    // start of phase B. Past the workgroup's last key tile the index is clamped to
+    // it: the reload lands in a buffer that is never read again.
+    load_k(stk, min(j + 2, j1 - 1));
 
     const int valid = tile_valid(j);
     if (valid < BN) {  // ragged last tile of a segment: drop keys past its end
@@ -281,7 +309,7 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by a slice
     // of the softmax of S_j: the row max, then the probabilities of P blocks 0 and 1.
     // At the last iteration the K buffer holds no tile and S_{j+1} is discarded.
-    const uint16_t* kb = kbuf[(j + 1) & 1];
+    const uint16_t* kb = kbuf[jb ^ 1];
     auto k_operand = [&](int i) {  // i = KS * mb + kk
       return *reinterpret_cast<const bf16x8*>(kb + k_lane + 32 * (i / KS) * KROW + 16 * (i % KS));
     };
@@ -344,8 +372,8 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
     // ---- phase B: O^T += V_j^T P_j^T, P block-major; the probabilities of P blocks
     // 2 and 3 are formed under the MFMAs of blocks 0 and 1. V^T operands come from
     // LDS transpose reads issued two MFMAs ahead.
-    load_v(stv, min(j + 1, nt - 1));
-    const uint16_t* vs = vbuf[j & 1];
+    load_v(stv, min(j + 1, j1 - 1));
+    const uint16_t* vs = vbuf[jb];
     auto v_operand = [&](int i) {  // i = DB * s2 + db
       const uint16_t* a = vs + v_lane + 16 * (i / DB) * VROW + 32 * (i % DB);
       const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(a));
@@ -378,17 +406,38 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
       l_ref = l_run;
       l_run = 0.f;
     }
-    stage_store<D, true>(stk, kbuf[j & 1], k_st);
-    stage_store<D, false>(stv, vbuf[(j + 1) & 1], v_st);
+    stage_store<D, true>(stk, kbuf[jb], k_st);
+    stage_store<D, false>(stv, vbuf[jb ^ 1], v_st);
     __syncthreads();
   };
 
-  int j = 0;
-  for (; j + 1 < nt; j += 2) {
+  int j = j0;
+  for (; j + 1 < j1; j += 2) {
     iteration(j, sa, sb);
     iteration(j + 1, sb, sa);
   }
-  if (j < nt) iteration(j, sa, sb);
+  if (j < j1) iteration(j, sa, sb);
+  if (j1 < n_rt) {  // a key chunk inside the reference segment: all of it is reference mass
+    m_ref = m_run;
+    l_ref = l_run;
+    l_run = 0.f;
+  }
+
+  // ---- epilogue of a key chunk: unnormalised output and statistics to the workspace
+  if (slot >= 0) {
+    if (qvalid) {
+      const int64_t prow = (int64_t)slot * BM + wave * 32 + n;
+      float* po = p.part_o + prow * D;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+          *reinterpret_cast<float4*>(po + 32 * db + 8 * rr + 4 * g) =
+              float4{o[db][4 * rr], o[db][4 * rr + 1], o[db][4 * rr + 2], o[db][4 * rr + 3]};
+      if (g == 0) p.part_st[prow] = float4{m_run, l_run, m_ref, l_ref};
+    }
+    return;
+  }
 
   // ---- epilogue
   const float L_R = l_ref > 0.f ? l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) : 0.f;
@@ -425,13 +474,115 @@ __global__ __launch_bounds__(NT, 2) void attn_bf16_kernel(AttnParams p) {
   }
 }
 
+// Combines the key chunks of split query tiles: one row per D/4 threads, four
+// output columns per thread. With M the largest running max over the chunks,
+//   L_R = sum_c l_R,c 2^(m_R,c - M),  L_Y = sum_c l_Y,c 2^(m_c - M),
+//   o = sum_c O_c 2^(m_c - M) / (L_R + L_Y),  mass = L_R / (L_R + L_Y).
+// A chunk's reference max never exceeds its running max, so M bounds both.
+template <int D>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  constexpr int TPR = D / 4, RPB = 256 / TPR;
+  bool tgt_only = false;
+  if (p.kvsrc == KV_DEVICE) tgt_only = __builtin_amdgcn_readfirstlane(*p.decision) == DEC_REUSE;
+  const SplitPlan pl = p.plan[tgt_only ? 1 : 0];
+  const int qt_ref = tgt_only ? 0 : p.qt_ref;
+  const int r = blockIdx.x * RPB + threadIdx.x / TPR, col = 4 * (threadIdx.x % TPR);
+  const int st = r / BM, rr = r - st * BM;
+  if (st >= pl.split_tiles) return;
+  const int tile = pl.whole + st;
+  const int qt_bh = qt_ref + p.qt_tgt;
+  const int bh = tile / qt_bh;
+  int qt = tile - bh * qt_bh;
+  const bool ref_rows = qt < qt_ref;
+  if (!ref_rows) qt -= qt_ref;
+  const int n_rows = ref_rows ? p.n_ref : p.n_tgt;
+  const int qrow = qt * BM + rr;
+  if (qrow >= n_rows) return;
+
+  const int64_t base = (int64_t)st * pl.chunks * BM + rr;  // partial row of chunk 0
+  float M = -__builtin_inff();
+  for (int c = 0; c < pl.chunks; ++c) M = fmaxf(M, p.part_st[base + (int64_t)c * BM].x);
+  float L_R = 0.f, L_Y = 0.f;
+  float4 acc{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < pl.chunks; ++c) {
+    const int64_t prow = base + (int64_t)c * BM;
+    const float4 sv = p.part_st[prow];
+    const float wgt = __builtin_amdgcn_exp2f(sv.x - M);
+    L_Y += sv.y * wgt;
+    if (sv.w > 0.f) L_R += sv.w * __builtin_amdgcn_exp2f(sv.z - M);
+    const float4 ov = *reinterpret_cast<const float4*>(p.part_o + prow * D + col);
+    acc.x += ov.x * wgt;
+    acc.y += ov.y * wgt;
+    acc.z += ov.z * wgt;
+    acc.w += ov.w * wgt;
+  }
+  const float total = L_R + L_Y;
+  const float inv = 1.f / total;
+  const View& ov = ref_rows ? p.o_ref : p.o_tgt;
+  const int b = bh / p.H, h = bh - b * p.H;
+  uint16_t* op = static_cast<uint16_t*>(const_cast<void*>(ov.p)) + b * ov.sb + h * ov.sh + (int64_t)qrow * ov.ss;
+  union {
+    __bf16 h[4];
+    u32x2 w;
+  } pk;
+  pk.h[0] = (__bf16)(acc.x * inv);
+  pk.h[1] = (__bf16)(acc.y * inv);
+  pk.h[2] = (__bf16)(acc.z * inv);
+  pk.h[3] = (__bf16)(acc.w * inv);
+  *reinterpret_cast<u32x2*>(op + col) = pk.w;
+  if (col == 0) {
+    const float mass = L_R * inv;
+    const int64_t row = (int64_t)bh * n_rows + qrow;
+    if (!ref_rows) {
+      if (p.mass_tgt) p.mass_tgt[row] = mass;
+      if (p.lse_tgt) {
+        const float ln2 = 0.69314718055994531f;
+        p.lse_tgt[2 * row] = (M + __log2f(L_R)) * ln2;
+        p.lse_tgt[2 * row + 1] = (M + __log2f(total)) * ln2;
+      }
+    } else if (p.mass_refq) {
+      p.mass_refq[row] = mass;
+    }
+  }
+}
+
 }  // namespace
 
+AttnSlots attn_bf16_slots(int head_dim) {
+  static std::atomic<int> cache[64][2][2];
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return AttnSlots{0, 0};
+  const int di = head_dim == 128 ? 1 : 0;
+  if (dev < 64) {
+    const int c = cache[dev][di][0].load(std::memory_order_relaxed);
+    if (c > 0) return AttnSlots{c, cache[dev][di][1].load(std::memory_order_relaxed)};
+  }
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return AttnSlots{0, 0};
+  const hipError_t e =
+      head_dim == 128
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<128>, NT, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<64>, NT, 0);
+  if (e != hipSuccess || per_cu < 1 || cus < 1) return AttnSlots{0, 0};
+  if (dev < 64) {
+    cache[dev][di][1].store(per_cu, std::memory_order_relaxed);
+    cache[dev][di][0].store(cus, std::memory_order_relaxed);
+  }
+  return AttnSlots{cus, per_cu};
+}
+
 hipError_t launch_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream) {
-  if (p.total_tiles <= 0) return hipSuccess;
-  const dim3 grid(p.total_tiles), block(NT);
-  return head_dim == 128 ? launch_kernel(attn_bf16_kernel<128>, grid, block, 0, stream, p)
-                         : launch_kernel(attn_bf16_kernel<64>, grid, block, 0, stream, p);
+  const int items = max(p.plan[0].total_items, p.plan[1].total_items);
+  if (items <= 0) return hipSuccess;
+  const dim3 grid(items), block(NT);
+  hipError_t e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128>, grid, block, 0, stream, p)
+                                 : launch_kernel(attn_bf16_kernel<64>, grid, block, 0, stream, p);
+  if (e != hipSuccess) return e;
+  const int split = max(p.plan[0].split_tiles, p.plan[1].split_tiles);
+  if (split == 0) return hipSuccess;
+  const int rpb = 256 / (head_dim / 4);
+  const dim3 mgrid((split * BM + rpb - 1) / rpb);
+  return head_dim == 128 ? launch_kernel(attn_merge_kernel<128>, mgrid, dim3(256), 0, stream, p)
+                         : launch_kernel(attn_merge_kernel<64>, mgrid, dim3(256), 0, stream, p);
 }
 
 }  // namespace refadapt

@@ -18,6 +18,18 @@ struct View {
 enum { KV_FRESH = 0, KV_CACHE = 1, KV_DEVICE = 2 };
 enum { DEC_REUSE = 0, DEC_REACTIVATE = 1, DEC_COMPUTE = 2 };
 
+// Work decomposition of one bf16 attention launch over its query tiles (all
+// tiles of a (batch, head) attend to every key tile, so they cost the same).
+// Launch indices [0, whole) run whole query tiles; the last `split_tiles`
+// query tiles are cut into `chunks` contiguous key-tile ranges each, launched
+// at [whole, total_items), whose partial results a merge kernel combines.
+struct SplitPlan {
+  int32_t whole;        // query tiles run whole (a multiple of the resident workgroup slots)
+  int32_t split_tiles;  // query tiles run in key chunks
+  int32_t chunks;       // key chunks per split tile (1 when split_tiles == 0)
+  int32_t total_items;  // whole + split_tiles * chunks (workgroups that do work)
+};
+
 struct AttnParams {
   View q_tgt, k_tgt, v_tgt;
   View q_ref, k_fresh, v_fresh, k_cache, v_cache;
@@ -32,12 +44,26 @@ struct AttnParams {
   int32_t total_tiles;  // B * H * (qt_ref + qt_tgt) = grid size
   int32_t kvsrc;
   float sc_log2;  // softmax scale * log2(e)
+  // bf16 path: plan[0] covers the launch's query set (under KV_DEVICE: every
+  // query tile), plan[1] the target query tiles alone (KV_DEVICE on REUSE).
+  SplitPlan plan[2];
+  float* part_o;     // [items][BM][head_dim] unnormalised fp32 partial outputs of split items
+  float4* part_st;   // [items][BM] (m, l_tgt, m_ref, l_ref) per partial row
 };
 
-// Query rows per workgroup of each attention kernel (the host sizes the grid with these).
-constexpr int kAttnBf16BM = 128;
+// Query rows per workgroup of each attention kernel (the host sizes the grid with
+// these) and keys per key tile of the bf16 kernel.
+constexpr int kAttnBf16BM = 256;
+constexpr int kAttnBf16BN = 64;
 constexpr int kAttnF32BM = 64;
 
+// Compute units of the current device and bf16 attention workgroups each holds
+// at once; zeros if the device cannot be queried.
+struct AttnSlots {
+  int cus, per_cu;
+};
+AttnSlots attn_bf16_slots(int head_dim);
+// Enqueues the bf16 attention kernel and, when a plan splits tiles, the merge.
 hipError_t launch_attn_bf16(const AttnParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_attn_f32(const AttnParams& p, int head_dim, hipStream_t stream);
 

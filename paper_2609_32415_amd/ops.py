@@ -85,11 +85,15 @@ def joint_attn(
     ref_mass=True,
     lse=False,
     ref_mass_refq=False,
+    workspace=None,
 ):
     """Joint attention over [K_R; K_Y] through ``refadapt_joint_attn``.
 
     ``ref_mass``/``lse``/``ref_mass_refq`` may be booleans (allocate when True)
-    or preallocated fp32 tensors. Returns an ``AttnOut``.
+    or preallocated fp32 tensors. ``workspace``: None allocates the key-split
+    workspace the library asks for (torch caching allocator), False runs
+    without key splits, a uint8 device tensor is used as given (see
+    ``attn_workspace``). Returns an ``AttnOut``.
     """
     B, H, n_tgt, D = q_tgt.shape
     dt = q_tgt.dtype
@@ -126,6 +130,14 @@ def joint_attn(
     shp_t = (B, H, n_tgt, D)
     shp_r = (B, H, n_ref, D)
     desc = L.ra_attn_desc(B, H, D, n_ref, n_tgt, _DTYPES[dt], float(scale or 0.0), _QSET[qset], _KVSRC[kvsrc])
+    if workspace is None:
+        nbytes = L.refadapt_joint_attn_workspace_size(desc)
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes else False
+    if workspace is False:
+        ws_ptr, ws_bytes = None, 0
+    else:
+        _on_gpu("workspace", workspace)
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     args = L.ra_attn_args(
         q_tgt=_view("q_tgt", q_tgt, dt, shp_t),
         k_tgt=_view("k_tgt", k_tgt, dt, shp_t),
@@ -141,9 +153,21 @@ def joint_attn(
         ref_mass=None if mass_t is None else mass_t.data_ptr(),
         lse_tgt=None if lse_t is None else lse_t.data_ptr(),
         ref_mass_refq=None if mrq_t is None else mrq_t.data_ptr(),
+        workspace=ws_ptr,
+        workspace_bytes=ws_bytes,
     )
     L.refadapt_joint_attn(desc, args, _stream())
     return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t)
+
+
+def attn_workspace(q_tgt, n_ref, qset="target", kvsrc="fresh"):
+    """Preallocated key-split workspace for ``joint_attn`` calls of this shape on
+    ``q_tgt``'s device (False when the library would not split)."""
+    B, H, n_tgt, D = q_tgt.shape
+    desc = L.ra_attn_desc(B, H, D, n_ref, n_tgt, _DTYPES[q_tgt.dtype], 0.0, _QSET[qset], _KVSRC[kvsrc])
+    with torch.cuda.device(q_tgt.device):
+        nbytes = L.refadapt_joint_attn_workspace_size(desc)
+    return torch.empty(nbytes, dtype=torch.uint8, device=q_tgt.device) if nbytes else False
 
 
 def q_change_workspace(q_tgt):

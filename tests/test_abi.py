@@ -63,6 +63,7 @@ def _args(**kw):
         ({}, dict(v_tgt=_t(ptr=0x1002)), L.RA_EUNSUPPORTED, "v_tgt"),
         ({}, dict(k_tgt=_t(ss=64)), L.RA_EINVAL, "row stride"),
         (dict(batch=0), {}, L.RA_EINVAL, "batch"),
+        ({}, dict(workspace=0x1008, workspace_bytes=1 << 20), L.RA_EUNSUPPORTED, "workspace"),
     ],
 )
 def test_joint_attn_rejects_bad_arguments(desc, args, status, msg):
@@ -75,6 +76,16 @@ def test_joint_attn_rejects_bad_arguments(desc, args, status, msg):
 
 def test_joint_attn_null_structs():
     assert L.LIB.refadapt_joint_attn(None, None, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_joint_attn(ctypes.byref(_desc()), None, None) == L.RA_EINVAL
+
+
+def test_joint_attn_workspace_size_needs_no_split_for_fp32_or_bad_descs():
+    """The fp32 path never splits key ranges, and a malformed desc asks for nothing
+    (refadapt_joint_attn reports its error instead)."""
+    assert L.refadapt_joint_attn_workspace_size(_desc(dtype=L.RA_F32, head_dim=64, n_ref=4096, n_tgt=4096)) == 0
+    assert L.refadapt_joint_attn_workspace_size(_desc(head_dim=96)) == 0
+    assert L.refadapt_joint_attn_workspace_size(_desc(n_tgt=0)) == 0
+    assert L.LIB.refadapt_joint_attn_workspace_size(None) == 0
 
 
 def test_q_change_validation():

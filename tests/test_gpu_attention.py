@@ -138,8 +138,9 @@ def test_unchanged_cache_equals_full_fresh_target_rows(dtype, d):
     """Reuse with cache == fresh reproduces the full-fresh target rows bit for bit."""
     _, x = _inputs(dtype, d, 200, 260, 1, 2)
     same = dict(x, k_ref_cache=x["k_ref"], v_ref_cache=x["v_ref"])
-    reuse = _gpu(same, dtype, "target", "cache")
-    full = _gpu(same, dtype, "all", "fresh")
+    # Without key splits both launches reduce each target row in the same order.
+    reuse = _gpu(same, dtype, "target", "cache", workspace=False)
+    full = _gpu(same, dtype, "all", "fresh", workspace=False)
     assert torch.equal(reuse.o_tgt, full.o_tgt)
     assert torch.equal(reuse.ref_mass, full.ref_mass)
 
@@ -155,6 +156,75 @@ def test_mass_outputs_do_not_change_o_and_runs_are_deterministic(dtype, d):
     torch.cuda.synchronize()
     assert torch.equal(a.o_tgt, b.o_tgt)
     assert torch.equal(b.o_tgt, c.o_tgt) and torch.equal(b.ref_mass, c.ref_mass) and torch.equal(b.lse, c.lse)
+
+
+# Shapes whose launches the host splits into key chunks of 4-5 key tiles (few
+# query tiles, many key tiles): chunks wholly inside the reference segment, a
+# chunk that spans the segment boundary through a ragged reference tile, a
+# chunk that ends exactly at the boundary (576 = 9 key tiles), no reference.
+SPLIT = [
+    # d, n_ref, n_tgt, H
+    (128, 1000, 100, 2),
+    (128, 576, 576, 2),
+    (128, 700, 300, 3),
+    (128, 0, 1100, 2),
+    (64, 1000, 100, 2),
+]
+
+
+def _workspace_bytes(n_ref, n_tgt, H, d, qset, kvsrc):
+    from paper_2609_32415_amd import _lib as L
+
+    desc = L.ra_attn_desc(1, H, d, n_ref, n_tgt, L.RA_BF16, 0.0, {"target": 0, "all": 1}[qset],
+                          {"fresh": 0, "cache": 1, "device": 2}[kvsrc])
+    return L.refadapt_joint_attn_workspace_size(desc)
+
+
+@pytest.mark.parametrize("case", SPLIT, ids=lambda c: "-".join(map(str, c)))
+@pytest.mark.parametrize("mode", [("target", "cache"), ("all", "fresh")], ids=lambda m: "/".join(m))
+def test_key_split_parity_all_elements(case, mode):
+    d, n_ref, n_tgt, H = case
+    qset, kvsrc = mode
+    print(f"key split bf16 d{d} n_ref {n_ref} n_tgt {n_tgt} H {H} {qset}/{kvsrc}", flush=True)
+    assert _workspace_bytes(n_ref, n_tgt, H, d, qset, kvsrc) > 0, "the launch should split key ranges"
+    _, x = _inputs("bf16", d, n_ref, n_tgt, 1, H)
+    ref = _oracle(x, qset, kvsrc == "cache")
+    got = _gpu(x, "bf16", qset, kvsrc)
+    whole = _gpu(x, "bf16", qset, kvsrc, workspace=False)
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    lse = host(got.lse)
+    if n_ref > 0:
+        assert max_abs(lse[..., 0], ref["tgt"]["lse_ref"]) <= 1e-3
+    else:
+        assert np.all(np.isneginf(lse[..., 0]))
+        assert np.all(host(got.ref_mass) == 0.0)
+    assert max_abs(lse[..., 1], ref["tgt"]["lse_all"]) <= 1e-3
+    assert max_abs(host(got.o_tgt), host(whole.o_tgt)) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), host(whole.ref_mass)) <= MASS_TOL["bf16"]
+    if qset == "all" and n_ref > 0:
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
+        assert max_abs(host(got.ref_mass_refq), ref["ref"]["ref_mass"]) <= MASS_TOL["bf16"]
+
+
+@pytest.mark.parametrize("decision", [0, 1, 2], ids=["REUSE", "REACTIVATE", "COMPUTE"])
+def test_key_split_device_mode_follows_decision_word(decision):
+    """Under RA_KV_DEVICE each decision has its own split plan, chosen on the device."""
+    print(f"key split device mode decision {decision}", flush=True)
+    n_ref, n_tgt, H = 1000, 100, 2
+    assert _workspace_bytes(n_ref, n_tgt, H, 128, "target", "device") > 0
+    _, x = _inputs("bf16", 128, n_ref, n_tgt, 1, H)
+    sentinel = 7.0
+    o_ref = torch.full((1, H, n_ref, 128), sentinel, dtype=torch.bfloat16, device="cuda:0")
+    dec = torch.tensor([decision], dtype=torch.int32, device="cuda:0")
+    got = _gpu(x, "bf16", "target", "device", decision=dec, o_ref=o_ref)
+    ref = _oracle(x, "all", decision != 2)
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    if decision == 0:
+        assert np.all(host(o_ref) == sentinel)
+    else:
+        assert max_abs(host(o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
 
 
 def test_custom_scale_and_strided_views():
