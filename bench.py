@@ -4,8 +4,9 @@ One step = one pass of the whole path over one block of the multi-reference
 image-editing workload (batch 1, 24 heads, head_dim 128, 4096 target tokens,
 3 x 4096 reference-image + 256 text tokens = 12544 reference tokens, bf16):
 
-  1. Q-change      D = ||Q_t - Q_{t-1}||_F / (||Q_{t-1}||_F + eps) per head
-  2. gate          head-mean D*M against theta, decision written on the device
+  1+2. Q-change and gate, one launch:
+                   D = ||Q_t - Q_{t-1}||_F / (||Q_{t-1}||_F + eps) per head, then the
+                   head-mean D*M against theta, decision written on the device
   3. reuse attn    target queries over [cached K_R; K_Y]      (0.838 TFLOP)
   4. full attn     all queries over [fresh K_R; K_Y]          (3.402 TFLOP)
   5. cache commit  fresh reference K/V -> cache if the decision is COMPUTE
@@ -163,6 +164,7 @@ def main():
     theta = torch.full((1,), 0.1 * 0.2, dtype=torch.float32, device=dev)
     state = ops.new_gate_state(dev)
     ws = ops.q_change_workspace(t["q_tgt"])
+    ws_qg = ops.q_change_gate_workspace(t["q_tgt"])
     d_out = torch.empty((B, H), dtype=torch.float32, device=dev)
     dec = torch.empty(1, dtype=torch.int32, device=dev)
     score = torch.empty(3, dtype=torch.float32, device=dev)
@@ -177,29 +179,27 @@ def main():
     ws_f = ops.attn_workspace(t["q_tgt"], n_ref, "all", "fresh")
 
     ev = lambda: torch.cuda.Event(enable_timing=True)
-    marks = {k: [] for k in ("qc", "gate", "reuse", "full", "commit")}
+    marks = {k: [] for k in ("qcg", "reuse", "full", "commit")}
 
     def step(record):
-        e = [ev() for _ in range(6)] if record else None
+        e = [ev() for _ in range(5)] if record else None
         if record:
             e[0].record()
-        ops.q_change(t["q_tgt"], q_prev, out=d_out, workspace=ws)
+        ops.q_change_gate(t["q_tgt"], q_prev, mass_prev, theta, state, 0, 1, "product", d_out=d_out,
+                          decision_out=dec, score_out=score, workspace=ws_qg)
         if record:
             e[1].record()
-        ops.gate(d_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec, score_out=score)
-        if record:
-            e[2].record()
         ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=cache_k, v_cache=cache_v, n_ref=n_ref,
                        qset="target", kvsrc="cache", o_tgt=o_tgt_r, ref_mass=mass_r, workspace=ws_r)
         if record:
-            e[3].record()
+            e[2].record()
         ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
                        qset="all", kvsrc="fresh", o_tgt=o_tgt_f, o_ref=o_ref_f, ref_mass=mass_f, workspace=ws_f)
         if record:
-            e[4].record()
+            e[3].record()
         ops.cache_commit(t["k_ref"], t["v_ref"], commit_k, commit_v, decision=dec)
         if record:
-            e[5].record()
+            e[4].record()
         return e
 
     for _ in range(args.warmup):
@@ -219,6 +219,22 @@ def main():
             marks[k].append(a.elapsed_time(b))
     ms = {k: float(np.mean(v)) for k, v in marks.items()}
     ms_per_step = total_ms / args.steps
+
+    # Outside the timed step: the separate Q-change and gate kernels the fused launch replaces.
+    def timed(fn, n=20):
+        for _ in range(3):
+            fn()
+        a, b = ev(), ev()
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    ms["qc"] = timed(lambda: ops.q_change(t["q_tgt"], q_prev, out=d_out, workspace=ws))
+    ms["gate"] = timed(lambda: ops.gate(d_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec,
+                                        score_out=score))
 
     f_reuse = attn_flops(H, n_tgt, n_ref + n_tgt, D, B)
     f_full = attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, D, B)
@@ -256,6 +272,8 @@ def main():
         },
         "reuse_block_attn_speedup": round(ms["full"] / ms["reuse"], 3),
         "small_kernels": {
+            "q_change_gate_us": round(ms["qcg"] * 1e3, 2),
+            "q_change_gate_gbs": round((qc_bytes + B * H * n_tgt * 4) / (ms["qcg"] * 1e-3) / 1e9, 1),
             "q_change_us": round(ms["qc"] * 1e3, 2),
             "q_change_gbs": round(qc_bytes / (ms["qc"] * 1e-3) / 1e9, 1),
             "gate_us": round(ms["gate"] * 1e3, 2),

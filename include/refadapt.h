@@ -208,6 +208,27 @@ ra_status refadapt_gate(int32_t batch, int32_t heads, int32_t n_tgt, int32_t blo
                         int32_t* decision_out, float* score_out, void* stream);
 
 /*
+ * refadapt_q_change_gate - refadapt_q_change and refadapt_gate fused.
+ *
+ * Computes d_out[b, h] exactly as refadapt_q_change (bitwise the same values)
+ * and then the decision of refadapt_gate for `block` at `step` (same
+ * bookkeeping, modes, theta layout and outputs). The mean lagged mass M_h is
+ * summed by the Q-change workgroups over their rows (fp32 within a workgroup,
+ * fp64 across workgroups in a fixed order), so the head reductions of both
+ * steps run on every CU and the whole step is two kernels instead of three.
+ *
+ * `workspace`: device memory of at least refadapt_q_change_gate_workspace_size
+ * bytes, 16-byte aligned; contents need no initialisation.
+ * Errors: as refadapt_q_change and refadapt_gate together.
+ */
+size_t refadapt_q_change_gate_workspace_size(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim);
+ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim, int32_t dtype,
+                                 ra_tensor q_cur, ra_tensor q_prev, float eps, int32_t block, int32_t step,
+                                 int32_t mode, const float* mass_prev, const float* theta, ra_gate_state* state,
+                                 float* d_out, int32_t* decision_out, float* score_out, void* workspace,
+                                 size_t ws_bytes, void* stream);
+
+/*
  * refadapt_cache_commit - refresh a block's reference K/V cache.
  *
  * Copies k_ref -> k_cache and v_ref -> v_cache ([B, H, n_ref, d]) when

@@ -38,6 +38,8 @@ EXPORTED = (
     "refadapt_q_change_workspace_size",
     "refadapt_q_change",
     "refadapt_gate",
+    "refadapt_q_change_gate_workspace_size",
+    "refadapt_q_change_gate",
     "refadapt_cache_commit",
     "refadapt_last_error",
     "refadapt_version",
@@ -121,6 +123,11 @@ def _load():
     lib.refadapt_q_change.restype = i32
     lib.refadapt_gate.argtypes = [i32, i32, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp]
     lib.refadapt_gate.restype = i32
+    lib.refadapt_q_change_gate_workspace_size.argtypes = [i32, i32, i32, i32]
+    lib.refadapt_q_change_gate_workspace_size.restype = ctypes.c_size_t
+    lib.refadapt_q_change_gate.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, i32, i32, i32,
+                                           vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.refadapt_q_change_gate.restype = i32
     lib.refadapt_cache_commit.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor, ra_tensor, vp, vp, i32, vp]
     lib.refadapt_cache_commit.restype = i32
     lib.refadapt_last_error.argtypes = []
@@ -158,6 +165,17 @@ def refadapt_q_change(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, 
 
 def refadapt_gate(batch, heads, n_tgt, block, step, mode, d_cur, mass_prev, theta, state, decision_out, score_out, stream):
     return _check(LIB.refadapt_gate(batch, heads, n_tgt, block, step, mode, d_cur, mass_prev, theta, state, decision_out, score_out, stream))
+
+
+def refadapt_q_change_gate_workspace_size(batch, heads, n_tgt, head_dim):
+    return int(LIB.refadapt_q_change_gate_workspace_size(batch, heads, n_tgt, head_dim))
+
+
+def refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block, step, mode, mass_prev,
+                           theta, state, d_out, decision_out, score_out, workspace, ws_bytes, stream):
+    return _check(LIB.refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block, step,
+                                             mode, mass_prev, theta, state, d_out, decision_out, score_out,
+                                             workspace, ws_bytes, stream))
 
 
 def refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, k_cache, v_cache, decision, age, step, stream):

@@ -3,10 +3,11 @@
 Per denoising step and block the executor enqueues, on the current stream and
 without any host synchronisation:
 
-  refadapt_q_change    D of this block's target Q against the recorded one
-  refadapt_gate        head-mean D*M against theta_b, decision written on the device
-                       (block 0 also does the step bookkeeping: step 0 and the
-                       bounded-age refresh make every block of the step compute)
+  refadapt_q_change_gate  D of this block's target Q against the recorded one and
+                       the head-mean D*M against theta_b, decision written on the
+                       device (block 0 also does the step bookkeeping: step 0 and
+                       the bounded-age refresh make every block of the step compute);
+                       two launches (fused=False: refadapt_q_change + refadapt_gate, three)
   refadapt_joint_attn  RA_KV_DEVICE: REUSE -> target queries over the cached
                        reference K/V; REACTIVATE -> all queries over the cache;
                        COMPUTE -> all queries over fresh K/V
@@ -39,7 +40,7 @@ class Controller:
     """Device-resident controller state and per-block buffers of one trajectory."""
 
     def __init__(self, n_blocks, n_steps, batch, heads, n_ref, n_tgt, head_dim, theta, delta_max=None,
-                 mode="product", theta_m=None, dtype=torch.bfloat16, device="cuda:0", eps=1e-8):
+                 mode="product", theta_m=None, dtype=torch.bfloat16, device="cuda:0", eps=1e-8, fused=True):
         self.nb, self.n_steps = n_blocks, n_steps
         self.shape_r = (batch, heads, n_ref, head_dim)
         self.shape_t = (batch, heads, n_tgt, head_dim)
@@ -65,16 +66,22 @@ class Controller:
         self.o_tgt = [torch.empty(self.shape_t, dtype=dtype, device=device) for _ in range(n_blocks)]
         self.o_ref = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
         q_like = torch.empty(self.shape_t, dtype=dtype, device=device)
-        self.ws = ops.q_change_workspace(q_like)
+        self.fused = fused
+        self.ws = ops.q_change_gate_workspace(q_like) if fused else ops.q_change_workspace(q_like)
         self.attn_ws = ops.attn_workspace(q_like, n_ref, kvsrc="device")
 
     def block(self, t, b, x):
         """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``."""
         q_prev = self.q_prev[b] if self.q_prev[b] is not None else x["q_tgt"]
-        ops.q_change(x["q_tgt"], q_prev, self.eps, out=self.d[b], workspace=self.ws)
         dec = self.decisions[t, b:b + 1]
-        ops.gate(self.d[b], self.mass[b][self.parity[b]], self.theta, self.state, b, t, self.mode,
-                 decision_out=dec, score_out=self.scores[t, b])
+        if self.fused:
+            ops.q_change_gate(x["q_tgt"], q_prev, self.mass[b][self.parity[b]], self.theta, self.state, b, t,
+                              self.mode, self.eps, d_out=self.d[b], decision_out=dec, score_out=self.scores[t, b],
+                              workspace=self.ws)
+        else:
+            ops.q_change(x["q_tgt"], q_prev, self.eps, out=self.d[b], workspace=self.ws)
+            ops.gate(self.d[b], self.mass[b][self.parity[b]], self.theta, self.state, b, t, self.mode,
+                     decision_out=dec, score_out=self.scores[t, b])
         nxt = 1 - self.parity[b]
         ops.joint_attn(
             x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"], v_ref=x["v_ref"],
@@ -123,15 +130,17 @@ def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=N
     return ctl, step_ms
 
 
-def run_sweep(device="cuda:0", w=None, log=None):
+def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.1, 0.2, 2), (0.1, 0.2, 4))):
     """The controller sweep (60 blocks x 8 steps, single-reference shapes).
 
     For each (theta_q, theta_m) cell the product gate runs with
-    theta = theta_q * theta_m (one threshold on the head-mean D*M score). Reports
-    the reuse fraction over steps >= 1, the attention-path time (Q-change, gate,
-    attention and commit kernels of every block) against a full-fresh trajectory
-    through the same harness (bounded-age refresh every step), and the relative
-    change of the executed target output against full-fresh attention.
+    theta = theta_q * theta_m (one threshold on the head-mean D*M score) and no
+    bounded-age refresh; ``delta_max_cells`` adds (theta_q, theta_m, delta_max)
+    cells with the refresh of Alg. 1 every delta_max steps. Reports the reuse
+    fraction over steps >= 1, the attention-path time (Q-change, gate, attention
+    and commit kernels of every block) against a full-fresh trajectory through
+    the same harness (bounded-age refresh every step), and the relative change of
+    the executed target output against full-fresh attention.
     """
     w = w or synth.workload("sweep")
     base, base_ms = _timed_run(w, device, 0.0, delta_max=1)
@@ -139,39 +148,39 @@ def run_sweep(device="cuda:0", w=None, log=None):
     if log:
         log(f"sweep: full-fresh trajectory {full_ms:.1f} ms")
     cells = []
-    for tq in w.theta_q:
-        for tm in w.theta_m:
-            theta = tq * tm
-            ctl, ms = _timed_run(w, device, theta, delta_max=None)
-            dec = ctl.decisions.cpu()
-            after0 = dec[1:]
-            errs = []
+    grid = [(tq, tm, None) for tq in w.theta_q for tm in w.theta_m] + list(delta_max_cells)
+    for tq, tm, dmax in grid:
+        theta = tq * tm
+        ctl, ms = _timed_run(w, device, theta, delta_max=dmax)
+        dec = ctl.decisions.cpu()
+        after0 = dec[1:]
+        errs = []
 
-            def keep(t, c, xs):  # untimed: relative change of executed vs full-fresh target output
-                for b in range(w.n_blocks):
-                    x = xs[b]
-                    fresh = ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_ref=x["k_ref"], v_ref=x["v_ref"],
-                                           ref_mass=False).o_tgt.float()
-                    diff = (c.o_tgt[b].float() - fresh).flatten(2).norm(dim=-1)
-                    errs.append((diff / (fresh.flatten(2).norm(dim=-1) + 1e-8)).flatten())
+        def keep(t, c, xs):  # untimed: relative change of executed vs full-fresh target output
+            for b in range(w.n_blocks):
+                x = xs[b]
+                fresh = ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_ref=x["k_ref"], v_ref=x["v_ref"],
+                                       ref_mass=False).o_tgt.float()
+                diff = (c.o_tgt[b].float() - fresh).flatten(2).norm(dim=-1)
+                errs.append((diff / (fresh.flatten(2).norm(dim=-1) + 1e-8)).flatten())
 
-            _timed_run(w, device, theta, delta_max=None, keep=keep)
-            e = torch.cat(errs).cpu()
-            cells.append({
-                "theta_q": tq, "theta_m": tm, "theta": theta,
-                "reuse_fraction": round(float((after0 == REUSE).float().mean()), 4),
-                "reuse_or_reactivate_fraction": round(float((after0 != COMPUTE).float().mean()), 4),
-                "attn_path_ms": round(sum(ms), 3),
-                "speedup_vs_full_fresh": round(full_ms / sum(ms), 3),
-                "boundary_block_per_step": [next((i for i, x in enumerate(row) if x == REACTIVATE), None)
-                                            for row in dec.tolist()],
-                "impact_mean": round(float(e.mean()), 5),
-                "impact_p99": round(float(e.quantile(0.99)), 5),
-                "impact_max": round(float(e.max()), 5),
-            })
-            if log:
-                log(f"sweep: cell theta_q={tq} theta_m={tm}: {cells[-1]['attn_path_ms']} ms, "
-                    f"speedup {cells[-1]['speedup_vs_full_fresh']}, reuse {cells[-1]['reuse_fraction']}")
+        _timed_run(w, device, theta, delta_max=dmax, keep=keep)
+        e = torch.cat(errs).cpu()
+        cells.append({
+            "theta_q": tq, "theta_m": tm, "theta": theta, "delta_max": dmax,
+            "reuse_fraction": round(float((after0 == REUSE).float().mean()), 4),
+            "reuse_or_reactivate_fraction": round(float((after0 != COMPUTE).float().mean()), 4),
+            "attn_path_ms": round(sum(ms), 3),
+            "speedup_vs_full_fresh": round(full_ms / sum(ms), 3),
+            "boundary_block_per_step": [next((i for i, x in enumerate(row) if x == REACTIVATE), None)
+                                        for row in dec.tolist()],
+            "impact_mean": round(float(e.mean()), 5),
+            "impact_p99": round(float(e.quantile(0.99)), 5),
+            "impact_max": round(float(e.max()), 5),
+        })
+        if log:
+            log(f"sweep: cell theta_q={tq} theta_m={tm} delta_max={dmax}: {cells[-1]['attn_path_ms']} ms, "
+                f"speedup {cells[-1]['speedup_vs_full_fresh']}, reuse {cells[-1]['reuse_fraction']}")
     return {
         "workload": f"{w.n_blocks} blocks x {w.n_steps} steps, batch {w.batch}, {w.heads} heads, head_dim "
                     f"{w.head_dim}, n_ref {w.n_ref}, n_tgt {w.n_tgt}",

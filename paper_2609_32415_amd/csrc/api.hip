@@ -293,6 +293,43 @@ ra_status refadapt_gate(int32_t batch, int32_t heads, int32_t n_tgt, int32_t blo
   return launch_status(e, "gate");
 }
 
+size_t refadapt_q_change_gate_workspace_size(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim) {
+  if (batch < 1 || heads < 1 || n_tgt < 1 || head_dim < 1) return 0;
+  return q_change_gate_workspace_bytes(batch, heads, n_tgt, head_dim);
+}
+
+ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim, int32_t dtype,
+                                 ra_tensor q_cur, ra_tensor q_prev, float eps, int32_t block, int32_t step,
+                                 int32_t mode, const float* mass_prev, const float* theta, ra_gate_state* state,
+                                 float* d_out, int32_t* decision_out, float* score_out, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  if (batch < 1 || heads < 1 || n_tgt < 1)
+    return fail(RA_EINVAL, "q_change_gate: batch, heads, n_tgt must be >= 1");
+  if ((int64_t)batch * heads > 8192) return fail(RA_EUNSUPPORTED, "q_change_gate: batch*heads must be <= 8192");
+  if (dtype != RA_BF16 && dtype != RA_F32) return fail(RA_EINVAL, "q_change_gate: unknown dtype %d", dtype);
+  if (head_dim < 1 || head_dim % (dtype == RA_BF16 ? 8 : 4) != 0)
+    return fail(RA_EUNSUPPORTED, "q_change_gate: head_dim %d must be a positive multiple of %d", head_dim,
+                dtype == RA_BF16 ? 8 : 4);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RA_EINVAL, "q_change_gate: eps must be finite and >= 0");
+  if (block < 0 || step < 0) return fail(RA_EINVAL, "q_change_gate: block and step must be >= 0");
+  if (mode < RA_GATE_PRODUCT || mode > RA_GATE_AND) return fail(RA_EINVAL, "q_change_gate: unknown mode %d", mode);
+  ra_status s;
+  if ((s = check_tensor("q_cur", q_cur, dtype, n_tgt, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("q_prev", q_prev, dtype, n_tgt, head_dim)) != RA_OK) return s;
+  if (!mass_prev || !theta || !state || !d_out || !decision_out || !score_out)
+    return fail(RA_EINVAL, "q_change_gate: null pointer argument");
+  const size_t need = refadapt_q_change_gate_workspace_size(batch, heads, n_tgt, head_dim);
+  if (workspace == nullptr || ws_bytes < need)
+    return fail(RA_EWORKSPACE, "q_change_gate: workspace needs %zu bytes (got %zu)", need, workspace ? ws_bytes : 0);
+  if ((reinterpret_cast<uintptr_t>(workspace) & 15) != 0)
+    return fail(RA_EUNSUPPORTED, "q_change_gate: workspace must be 16-byte aligned");
+  const hipError_t e = launch_q_change_gate(dtype, batch, heads, n_tgt, head_dim, view(q_cur), view(q_prev), eps,
+                                            block, step, mode, mass_prev, theta, reinterpret_cast<GateState*>(state),
+                                            d_out, decision_out, score_out, workspace,
+                                            static_cast<hipStream_t>(stream));
+  return launch_status(e, "q_change_gate");
+}
+
 ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int32_t head_dim, int32_t dtype,
                                 ra_tensor k_ref, ra_tensor v_ref, ra_tensor k_cache, ra_tensor v_cache,
                                 const int32_t* decision, int32_t* age, int32_t step, void* stream) {

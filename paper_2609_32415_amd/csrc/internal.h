@@ -78,6 +78,12 @@ hipError_t launch_gate(int32_t B, int32_t H, int32_t n_tgt, int32_t block, int32
                        const float* d_cur, const float* mass_prev, const float* theta, GateState* state,
                        int32_t* decision_out, float* score_out, hipStream_t stream);
 
+size_t q_change_gate_workspace_bytes(int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim);
+hipError_t launch_q_change_gate(int dtype, int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim, View cur, View prev,
+                                float eps, int32_t block, int32_t step, int32_t mode, const float* mass_prev,
+                                const float* theta, GateState* state, float* d_out, int32_t* decision_out,
+                                float* score_out, void* ws, hipStream_t stream);
+
 hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, View k_src,
                                View v_src, View k_dst, View v_dst, const int32_t* decision, int32_t* age,
                                int32_t step, hipStream_t stream);

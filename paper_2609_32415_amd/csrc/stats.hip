@@ -3,10 +3,12 @@
 //               (paper Sec. 3.1 consecutive-drift equation on post-RoPE target Q)
 //   gate      - head-mean interaction score and the block decision
 //               (Sec. 4 factorized-risk and depth-cutoff equations; Alg. 1)
+//   q_change_gate - both in two launches: every Q-change workgroup also sums the
+//               lagged mass over its rows; one workgroup then adds up and decides
 //   commit    - device-conditional refresh of a block's reference K/V cache
 //
-// All three are bandwidth- or latency-bound; they use 16-byte coalesced loads
-// and fixed-order reductions, so every result is bitwise reproducible.
+// All are bandwidth- or latency-bound; they use 16-byte coalesced loads and
+// fixed-order reductions, so every result is bitwise reproducible.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -31,15 +33,10 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// Pass 1: one workgroup sums (cur - prev)^2 and prev^2 over a chunk of rows of one (b, h).
+// Sums (cur - prev)^2 and prev^2 over rows [r0, r1) of one (b, h), returned to thread 0
+// in a fixed order (per-thread fp32, wavefront butterfly, then wavefronts in order).
 template <bool BF16>
-__global__ __launch_bounds__(QC_THREADS) void q_change_partial(View cur, View prev, int32_t H, int32_t n_rows,
-                                                               int32_t head_dim, int32_t chunks, float2* ws) {
-  const int bh = blockIdx.y;
-  const int b = bh / H, h = bh - b * H;
-  const int rows_per = (n_rows + chunks - 1) / chunks;
-  const int r0 = blockIdx.x * rows_per;
-  const int r1 = min(n_rows, r0 + rows_per);
+__device__ __forceinline__ float2 q_change_rows(View cur, View prev, int b, int h, int r0, int r1, int32_t head_dim) {
   const int vec = BF16 ? 8 : 4;  // elements per 16-byte load
   const int vpr = head_dim / vec;
   const int nvec = max(0, r1 - r0) * vpr;
@@ -84,15 +81,31 @@ __global__ __launch_bounds__(QC_THREADS) void q_change_partial(View cur, View pr
     red[1][wave] = sp;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float a = 0.f, c = 0.f;
+  float a = 0.f, c = 0.f;
 #pragma unroll
-    for (int w = 0; w < QC_THREADS / 64; ++w) {
-      a += red[0][w];
-      c += red[1][w];
-    }
-    ws[(int64_t)bh * chunks + blockIdx.x] = make_float2(a, c);
+  for (int w = 0; w < QC_THREADS / 64; ++w) {
+    a += red[0][w];
+    c += red[1][w];
   }
+  return make_float2(a, c);
+}
+
+// Rows [r0, r1) of one (b, h) of chunk blockIdx.x out of `chunks` equal row ranges.
+__device__ __forceinline__ int2 chunk_rows(int n_rows, int chunks) {
+  const int rows_per = (n_rows + chunks - 1) / chunks;
+  const int r0 = blockIdx.x * rows_per;
+  return make_int2(r0, min(n_rows, r0 + rows_per));
+}
+
+// Pass 1: one workgroup sums (cur - prev)^2 and prev^2 over a chunk of rows of one (b, h).
+template <bool BF16>
+__global__ __launch_bounds__(QC_THREADS) void q_change_partial(View cur, View prev, int32_t H, int32_t n_rows,
+                                                               int32_t head_dim, int32_t chunks, float2* ws) {
+  const int bh = blockIdx.y;
+  const int b = bh / H, h = bh - b * H;
+  const int2 rr = chunk_rows(n_rows, chunks);
+  const float2 v = q_change_rows<BF16>(cur, prev, b, h, rr.x, rr.y, head_dim);
+  if (threadIdx.x == 0) ws[(int64_t)bh * chunks + blockIdx.x] = v;
 }
 
 // Pass 2: per (b, h), add the chunk partials in order (fp64) and form D.
@@ -109,6 +122,50 @@ __global__ __launch_bounds__(256) void q_change_final(const float2* ws, int32_t 
   out[bh] = (float)(sqrt(a) / (sqrt(c) + (double)eps));
 }
 
+// Alg. 1 block branch on one thread: step bookkeeping at block 0 (step 0, or step -
+// a_full >= delta_max with delta_max > 0, is a full refresh: every block of the step
+// computes), then COMPUTE if an earlier block reactivated, else REACTIVATE when the
+// head-mean score reaches theta, else REUSE. d[i], m[i] are the Q-change and the mean
+// lagged mass of (b, h) pair i; the head means are taken in fp64 in index order.
+__device__ void gate_decide(int32_t BH, int32_t block, int32_t step, int32_t mode, const float* d, const float* m,
+                            const float* theta, GateState* st, int32_t* decision_out, float* score_out) {
+  if (block == 0) {
+    const bool full = step == 0 || (st->delta_max > 0 && step - st->a_full >= st->delta_max);
+    if (full) st->a_full = step;
+    st->reactivated = full ? 1 : 0;
+    st->step = step;
+  }
+  double sd = 0.0, sm = 0.0, sg = 0.0;
+  for (int i = 0; i < BH; ++i) {
+    const double di = d[i], mi = m[i];
+    sd += di;
+    sm += mi;
+    sg += di * mi;  // per-head product before the mean
+  }
+  const double dm = sd / BH, mm = sm / BH, gm = sg / BH;
+  int dec;
+  if (st->reactivated) {
+    dec = DEC_COMPUTE;
+  } else {
+    bool cross;
+    if (mode == 0) {
+      cross = gm >= (double)theta[block];
+    } else if (mode == 1) {
+      cross = dm >= (double)theta[block];
+    } else if (mode == 2) {
+      cross = mm >= (double)theta[block];
+    } else {
+      cross = dm >= (double)theta[2 * block] && mm >= (double)theta[2 * block + 1];
+    }
+    dec = cross ? DEC_REACTIVATE : DEC_REUSE;
+    if (cross) st->reactivated = 1;
+  }
+  *decision_out = dec;
+  score_out[0] = (float)dm;
+  score_out[1] = (float)mm;
+  score_out[2] = (float)gm;
+}
+
 constexpr int GATE_THREADS = 1024;
 
 __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t n_tgt, int32_t block, int32_t step,
@@ -116,18 +173,7 @@ __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t 
                                                             const float* theta, GateState* st, int32_t* decision_out,
                                                             float* score_out) {
   extern __shared__ float m_head[];  // [BH] mean lagged mass per (b, h)
-  __shared__ int s_react;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-  if (tid == 0) {
-    if (block == 0) {  // step bookkeeping of Alg. 1: full refresh at step 0 and after delta_max steps
-      const bool full = step == 0 || (st->delta_max > 0 && step - st->a_full >= st->delta_max);
-      if (full) st->a_full = step;
-      st->reactivated = full ? 1 : 0;
-      st->step = step;
-    }
-    s_react = st->reactivated;
-  }
 
   // Mean over target queries of the lagged per-query reference mass, one wavefront per
   // (b, h): 16-byte loads, four in flight per lane, then a fixed-order butterfly.
@@ -162,38 +208,59 @@ __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t 
     if (lane == 0) m_head[bh] = s / (float)n_tgt;
   }
   __syncthreads();
+  if (tid == 0) gate_decide(BH, block, step, mode, d_cur, m_head, theta, st, decision_out, score_out);
+}
 
-  if (tid == 0) {
-    double sd = 0.0, sm = 0.0, sg = 0.0;
-    for (int i = 0; i < BH; ++i) {
-      const double d = d_cur[i], m = m_head[i];
-      sd += d;
-      sm += m;
-      sg += d * m;  // per-head product before the mean
-    }
-    const double dm = sd / BH, mm = sm / BH, gm = sg / BH;
-    int dec;
-    if (s_react) {
-      dec = DEC_COMPUTE;
-    } else {
-      bool cross;
-      if (mode == 0) {
-        cross = gm >= (double)theta[block];
-      } else if (mode == 1) {
-        cross = dm >= (double)theta[block];
-      } else if (mode == 2) {
-        cross = mm >= (double)theta[block];
-      } else {
-        cross = dm >= (double)theta[2 * block] && mm >= (double)theta[2 * block + 1];
-      }
-      dec = cross ? DEC_REACTIVATE : DEC_REUSE;
-      if (cross) st->reactivated = 1;
-    }
-    *decision_out = dec;
-    score_out[0] = (float)dm;
-    score_out[1] = (float)mm;
-    score_out[2] = (float)gm;
+// Q-change and gate in two launches (instead of three). Pass 1: workgroup (chunk, bh)
+// sums the Q-change terms and the lagged mass over its rows. Pass 2 (one workgroup):
+// per (b, h) the chunks are added in chunk order in fp64, D is written, and the mean
+// mass and D feed the decision.
+template <bool BF16>
+__global__ __launch_bounds__(QC_THREADS) void q_change_mass_partial(View cur, View prev, int32_t H, int32_t n_rows,
+                                                                    int32_t head_dim, int32_t chunks,
+                                                                    const float* mass_prev, float4* part) {
+  __shared__ float red[QC_THREADS / 64];
+  const int bh = blockIdx.y;
+  const int b = bh / H, h = bh - b * H;
+  const int2 rr = chunk_rows(n_rows, chunks);
+  const float2 v = q_change_rows<BF16>(cur, prev, b, h, rr.x, rr.y, head_dim);
+  const float* mrow = mass_prev + (int64_t)bh * n_rows;
+  float sm = 0.f;
+  for (int i = rr.x + threadIdx.x; i < rr.y; i += QC_THREADS) sm += mrow[i];
+  sm = wave_sum(sm);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sm;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float msum = 0.f;
+#pragma unroll
+    for (int w = 0; w < QC_THREADS / 64; ++w) msum += red[w];
+    part[(int64_t)bh * chunks + blockIdx.x] = make_float4(v.x, v.y, msum, 0.f);
   }
+}
+
+constexpr int QG_THREADS = 256;
+
+__global__ __launch_bounds__(QG_THREADS) void q_change_gate_final(const float4* part, int32_t BH, int32_t chunks,
+                                                                  int32_t n_rows, float eps, int32_t block,
+                                                                  int32_t step, int32_t mode, const float* theta,
+                                                                  GateState* st, float* d_out, int32_t* decision_out,
+                                                                  float* score_out) {
+  extern __shared__ float s_dm[];  // [2 * BH]: D, then the mean lagged mass of each (b, h)
+  for (int i = threadIdx.x; i < BH; i += QG_THREADS) {
+    double a = 0.0, c = 0.0, ms = 0.0;
+    for (int k = 0; k < chunks; ++k) {
+      const float4 pk = part[(int64_t)i * chunks + k];
+      a += pk.x;
+      c += pk.y;
+      ms += pk.z;
+    }
+    const float dv = (float)(sqrt(a) / (sqrt(c) + (double)eps));
+    d_out[i] = dv;
+    s_dm[i] = dv;
+    s_dm[BH + i] = (float)(ms / n_rows);
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) gate_decide(BH, block, step, mode, s_dm, s_dm + BH, theta, st, decision_out, score_out);
 }
 
 constexpr int CC_THREADS = 256;
@@ -254,6 +321,29 @@ hipError_t launch_gate(int32_t B, int32_t H, int32_t n_tgt, int32_t block, int32
   const int bh = B * H;
   return launch_kernel(gate_kernel, dim3(1), dim3(GATE_THREADS), bh * sizeof(float), stream, bh, n_tgt, block, step,
                        mode, d_cur, mass_prev, theta, state, decision_out, score_out);
+}
+
+size_t q_change_gate_workspace_bytes(int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim) {
+  return (size_t)B * H * q_change_chunks(n_tgt, head_dim) * sizeof(float4);
+}
+
+hipError_t launch_q_change_gate(int dtype, int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim, View cur, View prev,
+                                float eps, int32_t block, int32_t step, int32_t mode, const float* mass_prev,
+                                const float* theta, GateState* state, float* d_out, int32_t* decision_out,
+                                float* score_out, void* ws, hipStream_t stream) {
+  const int chunks = q_change_chunks(n_tgt, head_dim);
+  const dim3 grid(chunks, B * H);
+  float4* part = static_cast<float4*>(ws);
+  const hipError_t e =
+      dtype == 0 ? launch_kernel(q_change_mass_partial<true>, grid, dim3(QC_THREADS), 0, stream, cur, prev, H, n_tgt,
+                                 head_dim, chunks, mass_prev, part)
+                 : launch_kernel(q_change_mass_partial<false>, grid, dim3(QC_THREADS), 0, stream, cur, prev, H, n_tgt,
+                                 head_dim, chunks, mass_prev, part);
+  if (e != hipSuccess) return e;
+  const int bh = B * H;
+  return launch_kernel(q_change_gate_final, dim3(1), dim3(QG_THREADS), 2 * (size_t)bh * sizeof(float), stream,
+                       static_cast<const float4*>(part), bh, chunks, n_tgt, eps, block, step, mode, theta, state, d_out,
+                       decision_out, score_out);
 }
 
 hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, View k_src,

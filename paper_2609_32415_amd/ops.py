@@ -228,6 +228,52 @@ def gate(d_cur, mass_prev, theta, state, block, step, mode="product", decision_o
     return decision_out, score_out
 
 
+def q_change_gate_workspace(q_tgt):
+    """Workspace of ``q_change_gate`` for Q of this shape."""
+    B, H, n, D = q_tgt.shape
+    nbytes = L.refadapt_q_change_gate_workspace_size(B, H, n, D)
+    return torch.empty(nbytes, dtype=torch.uint8, device=q_tgt.device)
+
+
+def q_change_gate(q_cur, q_prev, mass_prev, theta, state, block, step, mode="product", eps=1e-8, d_out=None,
+                  decision_out=None, score_out=None, workspace=None):
+    """Q-change and gate fused through ``refadapt_q_change_gate``;
+    returns (d [B, H], decision int32[1], scores fp32[3])."""
+    B, H, n, D = q_cur.shape
+    dt = q_cur.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q_cur.device
+    for name, t in (("mass_prev", mass_prev), ("theta", theta), ("state", state)):
+        _on_gpu(name, t)
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if tuple(mass_prev.shape) != (B, H, n) or mass_prev.dtype != torch.float32:
+        raise ValueError("mass_prev must be fp32 [B, H, n_tgt]")
+    if theta.dtype != torch.float32 or state.dtype != torch.int32 or state.numel() != 4:
+        raise ValueError("theta must be fp32 and state int32[4]")
+    need = 2 * (block + 1) if mode == "and" else block + 1
+    if theta.numel() < need:
+        raise ValueError(f"theta has {theta.numel()} entries; block {block} needs {need}")
+    if d_out is None:
+        d_out = torch.empty((B, H), dtype=torch.float32, device=dev)
+    if decision_out is None:
+        decision_out = torch.empty(1, dtype=torch.int32, device=dev)
+    if score_out is None:
+        score_out = torch.empty(3, dtype=torch.float32, device=dev)
+    if workspace is None:
+        workspace = q_change_gate_workspace(q_cur)
+    for name, t in (("d_out", d_out), ("decision_out", decision_out), ("score_out", score_out),
+                    ("workspace", workspace)):
+        _on_gpu(name, t)
+    L.refadapt_q_change_gate(
+        B, H, n, D, _DTYPES[dt], _view("q_cur", q_cur, dt), _view("q_prev", q_prev, dt, q_cur.shape), float(eps),
+        int(block), int(step), _GATE[mode], _ptr(mass_prev), _ptr(theta), _ptr(state), _ptr(d_out),
+        _ptr(decision_out), _ptr(score_out), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(),
+    )
+    return d_out, decision_out, score_out
+
+
 def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0):
     """Copy fresh reference K/V into the cache when ``decision`` is COMPUTE (or None)."""
     B, H, n_ref, D = k_ref.shape

@@ -100,6 +100,22 @@ def test_q_change_validation():
     assert st == L.RA_EINVAL and "eps" in L.refadapt_last_error()
 
 
+def test_q_change_gate_validation():
+    ws = L.refadapt_q_change_gate_workspace_size(1, 24, 4096, 128)
+    assert ws >= 24 * 16 and ws % 16 == 0
+    assert L.refadapt_q_change_gate_workspace_size(0, 1, 1, 1) == 0
+    p = ctypes.c_void_p(0x1000)
+    call = lambda **kw: L.LIB.refadapt_q_change_gate(
+        kw.get("B", 1), 24, 4096, 128, L.RA_BF16, _t(), kw.get("qp", _t()), 1e-8, 0, 0, kw.get("mode", 0),
+        kw.get("m", p), p, p, p, p, p, kw.get("ws", ctypes.c_void_p(0x2000)), kw.get("wsb", ws), None)
+    assert call(wsb=ws - 16) == L.RA_EWORKSPACE
+    assert call(ws=ctypes.c_void_p(0x2008)) == L.RA_EUNSUPPORTED
+    assert call(qp=_t(0)) == L.RA_EINVAL and "q_prev" in L.refadapt_last_error()
+    assert call(m=None) == L.RA_EINVAL
+    assert call(mode=7) == L.RA_EINVAL
+    assert call(B=0) == L.RA_EINVAL
+
+
 def test_gate_and_commit_validation():
     p = ctypes.c_void_p(0x1000)
     assert L.LIB.refadapt_gate(1, 24, 4096, 0, 0, 9, p, p, p, p, p, p, None) == L.RA_EINVAL

@@ -42,12 +42,12 @@ def _margin_ok(tr, theta):
     return np.all(np.abs(tr.g_mean - th[None, :])[mask] > 1e-3)
 
 
-def _run_gpu(theta, delta_max=None):
+def _run_gpu(theta, delta_max=None, fused=True):
     from paper_2609_32415_amd.controller import Controller
 
     x = _x()
     ctl = Controller(W.n_blocks, W.n_steps, W.batch, W.heads, W.n_ref, W.n_tgt, W.head_dim, theta,
-                     delta_max=delta_max, device="cuda:0")
+                     delta_max=delta_max, device="cuda:0", fused=fused)
     outs, masses, ages = {}, {}, []
     for t in range(W.n_steps):
         xs = [{k: dev(v, "bf16") for k, v in x[(t, b)].items()} for b in range(W.n_blocks)]
@@ -65,14 +65,15 @@ CASES = [(0.02, None), (0.058, None), (0.105, None), (0.115, None), (0.05, 2), (
          (PER_BLOCK, None)]
 
 
+@pytest.mark.parametrize("fused", [True, False], ids=["fused", "separate"])
 @pytest.mark.parametrize("theta,delta_max", CASES, ids=lambda v: str(v))
-def test_controller_matches_oracle(theta, delta_max):
-    print(f"controller theta={theta} delta_max={delta_max}", flush=True)
+def test_controller_matches_oracle(theta, delta_max, fused):
+    print(f"controller theta={theta} delta_max={delta_max} fused={fused}", flush=True)
     x = _x()
     ref = run_controller(lambda t, b: x[(t, b)], W.n_steps, W.n_blocks, theta, delta_max=delta_max, keep_outputs=True)
     if not _margin_ok(ref, theta):
         pytest.skip("a head-mean score lies within 1e-3 of theta for this seed")
-    dec, outs, masses, ages = _run_gpu(theta, delta_max)
+    dec, outs, masses, ages = _run_gpu(theta, delta_max, fused)
     assert dec.tolist() == ref.decisions.tolist()
     assert ages.tolist() == ref.ages.tolist()
     for (t, b), o in outs.items():

@@ -113,6 +113,55 @@ def test_gate_sequence_matches_oracle(mode):
         assert st[1] == a_full and st[3] == t
 
 
+@pytest.mark.parametrize("mode", ["product", "and"])
+@pytest.mark.parametrize("dtype,B,H,n,d", [("bf16", 1, 24, 4096, 128), ("bf16", 2, 3, 333, 64), ("f32", 1, 2, 100, 64)])
+def test_fused_q_change_gate_matches_oracle(mode, dtype, B, H, n, d):
+    """refadapt_q_change_gate over steps x blocks with one reused workspace: D equals
+    refadapt_q_change bit for bit, decisions and scores follow the oracle's Q-change
+    and gate on the same inputs."""
+    print(f"q_change_gate {mode} {dtype} {B}x{H}x{n}x{d}", flush=True)
+    n_blocks, n_steps = 4, 3
+    rng = np.random.default_rng(7)
+    if mode == "and":
+        th = np.stack([rng.uniform(0.2, 0.4, n_blocks), rng.uniform(0.3, 0.6, n_blocks)], 1).astype(np.float32)
+    else:
+        th = rng.uniform(0.1, 0.2, n_blocks).astype(np.float32)
+    theta = torch.from_numpy(th.reshape(-1)).cuda()
+    state = ops.new_gate_state("cuda:0", delta_max=2)
+    q0 = synth.round_to_dtype(rng.standard_normal((B, H, n, d)).astype(np.float32), dtype)
+    ws = ops.q_change_gate_workspace(dev(q0, dtype))
+    a_full = 0
+    for t in range(n_steps):
+        full = full_refresh_due(t, a_full, 2)
+        if full:
+            a_full = t
+        react = full
+        for b in range(n_blocks):
+            sig = rng.uniform(0.05, 0.6, (1, H, 1, 1)).astype(np.float32)
+            q1 = synth.round_to_dtype(q0 + sig * rng.standard_normal(q0.shape).astype(np.float32), dtype)
+            m = rng.uniform(0.0, 1.0, (B, H, n)).astype(np.float32)
+            d_got, dec, score = ops.q_change_gate(dev(q1, dtype), dev(q0, dtype), dev(m, "f32"), theta, state, b, t,
+                                                  mode, workspace=ws)
+            d_ref = ops.q_change(dev(q1, dtype), dev(q0, dtype))
+            torch.cuda.synchronize()
+            assert torch.equal(d_got, d_ref)
+            dq = q_change(q1, q0)
+            np.testing.assert_allclose(host(d_got), dq, rtol=1e-5)
+            thr = float(th[b][0] if mode == "and" else th[b])
+            exp = gate(dq, m, thr, react, mode=mode, theta_m=float(th[b][1]) if mode == "and" else None)
+            react = exp.reactivated
+            got = int(dec.item())
+            margin = exp.g_mean if mode == "product" else exp.d_mean
+            if abs(margin - thr) > 1e-4 and (mode != "and" or abs(exp.m_mean - float(th[b][1])) > 1e-4):
+                assert got == exp.decision, (t, b, NAMES[got], NAMES[exp.decision])
+            else:
+                react = got != REUSE
+            np.testing.assert_allclose(host(score), [exp.d_mean, exp.m_mean, exp.g_mean], rtol=1e-5, atol=1e-7)
+            q0 = q1
+        st = state.cpu().tolist()
+        assert st[1] == a_full and st[3] == t
+
+
 def test_gate_thresholds_zero_and_infinite():
     B, H, n = 1, 4, 300
     d, m = _gate_inputs(5, B, H, n)
