@@ -103,6 +103,46 @@ class Controller:
         return self.mass[b][self.parity[b]]
 
 
+class StepGraphs:
+    """HIP graphs of every step of one controller trajectory.
+
+    Step t is captured once, from the controller's own per-block enqueues, as a
+    graph that reads its fresh inputs from static per-block buffers
+    ``inputs(t)`` (two sets, alternating with the step's parity, so step t's
+    recorded target Q is still in place when step t+1 reads it). Replaying
+    graphs 0..n_steps-1 in order runs the trajectory again: step 0's gate
+    bookkeeping re-initialises the device state, so a new trajectory needs no
+    reset. Capture must happen before any eager step of ``ctl`` (the captured
+    pointers follow its ping-pong state from step 0). ``make_inputs()`` returns
+    one list of per-block dicts of device tensors; it is called twice.
+    """
+
+    def __init__(self, ctl, make_inputs):
+        self.ctl = ctl
+        self.bufs = [make_inputs(), make_inputs()]
+        self.graphs = []
+        self._parity = []  # per step: the mass buffer each block's graph writes
+        torch.cuda.synchronize()
+        for t in range(ctl.n_steps):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                ctl.step(t, self.bufs[t % 2])
+            self.graphs.append(g)
+            self._parity.append(list(ctl.parity))
+        torch.cuda.synchronize()
+
+    def inputs(self, t):
+        """Static input buffers read by step t's graph (fill them before replay(t))."""
+        return self.bufs[t % 2]
+
+    def replay(self, t):
+        self.graphs[t].replay()
+
+    def recorded_mass(self, t, b):
+        """Per-query reference mass that block b's attention records at step t."""
+        return self.ctl.mass[b][self._parity[t][b]]
+
+
 def _sweep_inputs(w, device):
     trajs = [synth.DeviceTrajectory(w, b, device, ref_sigma=(lambda t, b=b: synth.sweep_ref_drift(b, w.n_blocks)),
                                     tgt_sigma=(lambda t: synth.sweep_tgt_drift(t, w.n_steps)))
@@ -130,7 +170,33 @@ def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=N
     return ctl, step_ms
 
 
-def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.1, 0.2, 2), (0.1, 0.2, 4))):
+def _graph_timed_run(w, device, theta, delta_max):
+    """As _timed_run, with every step replayed from a captured HIP graph."""
+    ctl = Controller(w.n_blocks, w.n_steps, w.batch, w.heads, w.n_ref, w.n_tgt, w.head_dim, theta,
+                     delta_max=delta_max, device=device)
+    trajs = _sweep_inputs(w, device)
+    shapes = {"q_tgt": ctl.shape_t, "k_tgt": ctl.shape_t, "v_tgt": ctl.shape_t,
+              "q_ref": ctl.shape_r, "k_ref": ctl.shape_r, "v_ref": ctl.shape_r}
+    graphs = StepGraphs(ctl, lambda: [{n: torch.empty(sh, dtype=torch.bfloat16, device=device)
+                                       for n, sh in shapes.items()} for _ in range(w.n_blocks)])
+    step_ms = []
+    for t in range(w.n_steps):
+        for b, buf in enumerate(graphs.inputs(t)):
+            x = trajs[b].step_tensors(t)
+            for n, v in buf.items():
+                v.copy_(x[n])
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        graphs.replay(t)
+        e1.record()
+        torch.cuda.synchronize()
+        step_ms.append(e0.elapsed_time(e1))
+    return ctl, step_ms
+
+
+def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2), (0.2, 0.4, 4)),
+              graph_cells=((0.2, 0.4),)):
     """The controller sweep (60 blocks x 8 steps, single-reference shapes).
 
     For each (theta_q, theta_m) cell the product gate runs with
@@ -174,6 +240,7 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.1, 0.2, 2),
             "speedup_vs_full_fresh": round(full_ms / sum(ms), 3),
             "boundary_block_per_step": [next((i for i, x in enumerate(row) if x == REACTIVATE), None)
                                         for row in dec.tolist()],
+            "decisions": dec.tolist(),
             "impact_mean": round(float(e.mean()), 5),
             "impact_p99": round(float(e.quantile(0.99)), 5),
             "impact_max": round(float(e.max()), 5),
@@ -181,7 +248,22 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.1, 0.2, 2),
         if log:
             log(f"sweep: cell theta_q={tq} theta_m={tm} delta_max={dmax}: {cells[-1]['attn_path_ms']} ms, "
                 f"speedup {cells[-1]['speedup_vs_full_fresh']}, reuse {cells[-1]['reuse_fraction']}")
+    # The same trajectories replayed from captured HIP graphs (one graph per step).
+    g_base, g_base_ms = _graph_timed_run(w, device, 0.0, delta_max=1)
+    graph = {"full_fresh_attn_path_ms": round(sum(g_base_ms), 3), "cells": []}
+    for tq, tm in graph_cells:
+        g_ctl, g_ms = _graph_timed_run(w, device, tq * tm, delta_max=None)
+        eager = next(c for c in cells if c["theta_q"] == tq and c["theta_m"] == tm and c["delta_max"] is None)
+        same = bool(torch.equal(g_ctl.decisions.cpu(), torch.tensor(eager["decisions"], dtype=torch.int32)))
+        graph["cells"].append({"theta_q": tq, "theta_m": tm, "attn_path_ms": round(sum(g_ms), 3),
+                               "speedup_vs_full_fresh": round(sum(g_base_ms) / sum(g_ms), 3),
+                               "decisions_equal_eager": same})
+    if log:
+        log(f"sweep: graph replay full-fresh {graph['full_fresh_attn_path_ms']} ms, cells {graph['cells']}")
+    for c in cells:
+        c.pop("decisions")
     return {
+        "graph_replay": graph,
         "workload": f"{w.n_blocks} blocks x {w.n_steps} steps, batch {w.batch}, {w.heads} heads, head_dim "
                     f"{w.head_dim}, n_ref {w.n_ref}, n_tgt {w.n_tgt}",
         "full_fresh_attn_path_ms": round(full_ms, 3),
