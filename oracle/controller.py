@@ -19,6 +19,12 @@ loop exercises exactly the parts of Alg. 1 that act on attention:
 * every block records its target Q and the realised target->reference mass
   of the attention it executed, for the next step.
 
+``cue="anchor"`` replaces the target-side cue by the change from the block's
+most recent materialisation anchor (App. C, anchor-relative target-Q change):
+D is measured against the target Q the block had at its last COMPUTE step
+a_b, not at the previous step; the gate is otherwise the same (the paper's
+Anchor-Q x Exposure ablation).
+
 Reading taken where the paper relies on the DiT: at the boundary block the
 paper restores the cached reference hidden state and recomputes the
 reference rows from it; without a DiT, the reference K/V at the boundary are
@@ -68,6 +74,7 @@ def run_controller(
     eps=1e-8,
     scale=None,
     keep_outputs=False,
+    cue="consecutive",
 ):
     """Run Alg. 1 and return a ``ControllerTrace``.
 
@@ -75,6 +82,8 @@ def run_controller(
     v_tgt`` arrays of shape ``[B, H, n, d]`` (the fresh tensors of block ``b``
     at step ``t``). ``theta`` is a scalar or a per-block sequence.
     """
+    if cue not in ("consecutive", "anchor"):
+        raise ValueError(f"unknown cue {cue!r}")
     theta = np.broadcast_to(np.asarray(theta, dtype=np.float64), (n_blocks,))
     theta_m_arr = None
     if theta_m is not None:
@@ -91,6 +100,7 @@ def run_controller(
     cache_k = [None] * n_blocks
     cache_v = [None] * n_blocks
     q_rec = [None] * n_blocks
+    q_anchor = [None] * n_blocks  # target Q at the block's last COMPUTE step
     mass_rec = [None] * n_blocks
     age = np.zeros(n_blocks, dtype=np.int64)
     a_full = 0
@@ -109,7 +119,7 @@ def run_controller(
             if full:
                 dec = COMPUTE
             else:
-                d = q_change(x["q_tgt"], q_rec[b], eps)
+                d = q_change(x["q_tgt"], q_anchor[b] if cue == "anchor" else q_rec[b], eps)
                 res = gate(
                     d,
                     mass_rec[b],
@@ -128,6 +138,7 @@ def run_controller(
                 mass_tgt = ex["ref_mass"][..., n_ref:]
                 cache_k[b] = np.array(x["k_ref"], dtype=np.float64)
                 cache_v[b] = np.array(x["v_ref"], dtype=np.float64)
+                q_anchor[b] = np.array(x["q_tgt"], dtype=np.float64)
                 age[b] = t
             elif dec == REACTIVATE:
                 ex = joint_attention(q_all, cache_k[b], cache_v[b], x["k_tgt"], x["v_tgt"], scale)

@@ -47,6 +47,25 @@ def test_hand_scenario():
     assert tr2.ages.tolist() == case["ages_delta_max_2"]
 
 
+def test_anchor_cue_closed_form():
+    """Target Q_t = (1 + 0.1 t) Q0 under exactly uniform attention (mass 2/8 = 1/4).
+    Consecutive change shrinks (0.1 / (1 + 0.1 (t-1))), so with theta = 0.04 every
+    block reuses after step 0. Anchor change grows with the distance to the last
+    COMPUTE step a (0.1 (t - a) / (1 + 0.1 a)): block 0 reaches 0.2 * 1/4 = 0.05 at
+    step 2 and reactivates, block 1 then computes and moves its anchor to the step."""
+    case = {"n_ref": 2, "n_tgt": 6, "c": [[1.0 + 0.1 * t] * 2 for t in range(4)]}
+    C, R, U = COMPUTE, REACTIVATE, REUSE
+    cons = run_controller(_scaled_inputs(case), 4, 2, 0.04, eps=0.0)
+    assert cons.decisions.tolist() == [[C, C], [U, U], [U, U], [U, U]]
+    np.testing.assert_allclose(cons.d_mean[1:, 0], [0.1, 0.1 / 1.1, 0.1 / 1.2], rtol=1e-12)
+    anc = run_controller(_scaled_inputs(case), 4, 2, 0.04, eps=0.0, cue="anchor")
+    assert anc.decisions.tolist() == [[C, C], [U, U], [R, C], [R, C]]
+    assert anc.ages.tolist() == [[0, 0], [0, 0], [0, 2], [0, 3]]
+    np.testing.assert_allclose(anc.d_mean[1:, 0], [0.1, 0.2, 0.3], rtol=1e-12)
+    np.testing.assert_allclose(anc.g_mean[1:, 0], [0.025, 0.05, 0.075], rtol=1e-12)
+    assert np.isnan(anc.d_mean[2, 1]) and np.isnan(anc.d_mean[3, 1])  # not read past the boundary
+
+
 def _random_inputs(seed, n_ref=6, n_tgt=5, heads=3, d=4, drift=0.2):
     base = {r: np.random.default_rng([seed, i]).standard_normal((1, heads, n_ref if r.endswith("ref") else n_tgt, d)) for i, r in enumerate(("q_ref", "k_ref", "v_ref", "q_tgt", "k_tgt", "v_tgt"))}
     cache = {}
