@@ -235,6 +235,8 @@ ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, in
  * `decision` is NULL or *decision == RA_COMPUTE, and then writes `step` to
  * *age when age is non-NULL (Alg. 1: a computing block updates its cached
  * K/V and sets its materialisation step a_b). Otherwise nothing is written.
+ * With v_ref and v_cache both of NULL data only k_ref -> k_cache is copied
+ * (e.g. the target Q kept as the block's materialisation anchor).
  * Errors: RA_EINVAL (null tensors, sizes), RA_EUNSUPPORTED (alignment).
  */
 ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int32_t head_dim, int32_t dtype,

@@ -15,7 +15,10 @@ without any host synchronisation:
 
 and records the block's target Q (by reference) and the per-query reference
 mass of the attention it executed (ping-pong buffers) for the next step. The
-decisions stay on the device until the caller reads them.
+decisions stay on the device until the caller reads them. With
+cue="anchor" the Q-change is taken against the target Q of the block's last
+COMPUTE step (copied on the device by a K-only commit), the paper's
+Anchor-Q x Exposure ablation.
 
 The block inputs are exogenous here: the caller supplies each block's fresh
 Q/K/V per step (the diffusion transformer whose hidden states would produce
@@ -40,7 +43,8 @@ class Controller:
     """Device-resident controller state and per-block buffers of one trajectory."""
 
     def __init__(self, n_blocks, n_steps, batch, heads, n_ref, n_tgt, head_dim, theta, delta_max=None,
-                 mode="product", theta_m=None, dtype=torch.bfloat16, device="cuda:0", eps=1e-8, fused=True):
+                 mode="product", theta_m=None, dtype=torch.bfloat16, device="cuda:0", eps=1e-8, fused=True,
+                 cue="consecutive"):
         self.nb, self.n_steps = n_blocks, n_steps
         self.shape_r = (batch, heads, n_ref, head_dim)
         self.shape_t = (batch, heads, n_tgt, head_dim)
@@ -59,6 +63,12 @@ class Controller:
                      for _ in range(n_blocks)]
         self.parity = [0] * n_blocks
         self.q_prev = [None] * n_blocks
+        if cue not in ("consecutive", "anchor"):
+            raise ValueError(f"unknown cue {cue!r}")
+        self.cue = cue
+        # anchor cue: the target Q of each block's last COMPUTE step
+        self.q_anchor = ([torch.empty(self.shape_t, dtype=dtype, device=device) for _ in range(n_blocks)]
+                         if cue == "anchor" else None)
         self.age = torch.zeros(n_blocks, dtype=torch.int32, device=device)
         self.d = torch.zeros((n_blocks, batch, heads), dtype=torch.float32, device=device)
         self.decisions = torch.full((n_steps, n_blocks), -1, dtype=torch.int32, device=device)
@@ -72,7 +82,10 @@ class Controller:
 
     def block(self, t, b, x):
         """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``."""
-        q_prev = self.q_prev[b] if self.q_prev[b] is not None else x["q_tgt"]
+        if self.cue == "anchor":
+            q_prev = self.q_anchor[b] if t > 0 else x["q_tgt"]
+        else:
+            q_prev = self.q_prev[b] if self.q_prev[b] is not None else x["q_tgt"]
         dec = self.decisions[t, b:b + 1]
         if self.fused:
             ops.q_change_gate(x["q_tgt"], q_prev, self.mass[b][self.parity[b]], self.theta, self.state, b, t,
@@ -90,6 +103,8 @@ class Controller:
         )
         ops.cache_commit(x["k_ref"], x["v_ref"], self.k_cache[b], self.v_cache[b], decision=dec,
                          age=self.age[b:b + 1], step=t)
+        if self.cue == "anchor":
+            ops.cache_commit(x["q_tgt"], None, self.q_anchor[b], None, decision=dec)
         self.q_prev[b] = x["q_tgt"]
         self.parity[b] = nxt
 
@@ -150,10 +165,10 @@ def _sweep_inputs(w, device):
     return trajs
 
 
-def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=None):
+def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=None, cue="consecutive"):
     """One trajectory; returns (controller, per-step attention-path milliseconds)."""
     ctl = Controller(w.n_blocks, w.n_steps, w.batch, w.heads, w.n_ref, w.n_tgt, w.head_dim, theta,
-                     delta_max=delta_max, mode=mode, theta_m=theta_m, device=device)
+                     delta_max=delta_max, mode=mode, theta_m=theta_m, device=device, cue=cue)
     trajs = _sweep_inputs(w, device)
     step_ms = []
     for t in range(w.n_steps):
@@ -168,6 +183,39 @@ def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=N
         torch.cuda.synchronize()
         step_ms.append(e0.elapsed_time(e1))
     return ctl, step_ms
+
+
+def _cell(w, device, full_ms, theta, delta_max=None, mode="product", theta_m=None, cue="consecutive"):
+    """One controller configuration: timed trajectory, then an untimed replay that
+    measures the executed target output's relative change against full-fresh attention."""
+    ctl, ms = _timed_run(w, device, theta, delta_max, mode, theta_m, cue=cue)
+    dec = ctl.decisions.cpu()
+    after0 = dec[1:]
+    errs = []
+
+    def keep(t, c, xs):  # untimed: relative change of executed vs full-fresh target output
+        for b in range(w.n_blocks):
+            x = xs[b]
+            fresh = ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_ref=x["k_ref"], v_ref=x["v_ref"],
+                                   ref_mass=False).o_tgt.float()
+            diff = (c.o_tgt[b].float() - fresh).flatten(2).norm(dim=-1)
+            errs.append((diff / (fresh.flatten(2).norm(dim=-1) + 1e-8)).flatten())
+
+    _timed_run(w, device, theta, delta_max, mode, theta_m, keep=keep, cue=cue)
+    e = torch.cat(errs).cpu()
+    return {
+        "mode": mode, "cue": cue, "theta": theta, "theta_m": theta_m, "delta_max": delta_max,
+        "reuse_fraction": round(float((after0 == REUSE).float().mean()), 4),
+        "reuse_or_reactivate_fraction": round(float((after0 != COMPUTE).float().mean()), 4),
+        "attn_path_ms": round(sum(ms), 3),
+        "speedup_vs_full_fresh": round(full_ms / sum(ms), 3),
+        "boundary_block_per_step": [next((i for i, x in enumerate(row) if x == REACTIVATE), None)
+                                    for row in dec.tolist()],
+        "decisions": dec.tolist(),
+        "impact_mean": round(float(e.mean()), 5),
+        "impact_p99": round(float(e.quantile(0.99)), 5),
+        "impact_max": round(float(e.max()), 5),
+    }
 
 
 def _graph_timed_run(w, device, theta, delta_max):
@@ -196,7 +244,7 @@ def _graph_timed_run(w, device, theta, delta_max):
 
 
 def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2), (0.2, 0.4, 4)),
-              graph_cells=((0.2, 0.4),)):
+              graph_cells=((0.2, 0.4),), ablation_cells=((0.05, 0.1), (0.1, 0.2), (0.2, 0.4))):
     """The controller sweep (60 blocks x 8 steps, single-reference shapes).
 
     For each (theta_q, theta_m) cell the product gate runs with
@@ -206,7 +254,12 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2),
     fraction over steps >= 1, the attention-path time (Q-change, gate, attention
     and commit kernels of every block) against a full-fresh trajectory through
     the same harness (bounded-age refresh every step), and the relative change of
-    the executed target output against full-fresh attention.
+    the executed target output against full-fresh attention. ``ablation_cells``
+    runs the cue ablation at those (theta_q, theta_m) pairs: Q-change alone
+    (theta_q), mass alone (theta_m), both with separate thresholds, the product,
+    the anchor-relative Q-change times mass, and a fixed refresh every 3 steps.
+    ``graph_cells`` repeats cells (and the full-fresh baseline) as HIP-graph
+    replays of captured steps.
     """
     w = w or synth.workload("sweep")
     base, base_ms = _timed_run(w, device, 0.0, delta_max=1)
@@ -216,38 +269,39 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2),
     cells = []
     grid = [(tq, tm, None) for tq in w.theta_q for tm in w.theta_m] + list(delta_max_cells)
     for tq, tm, dmax in grid:
-        theta = tq * tm
-        ctl, ms = _timed_run(w, device, theta, delta_max=dmax)
-        dec = ctl.decisions.cpu()
-        after0 = dec[1:]
-        errs = []
-
-        def keep(t, c, xs):  # untimed: relative change of executed vs full-fresh target output
-            for b in range(w.n_blocks):
-                x = xs[b]
-                fresh = ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_ref=x["k_ref"], v_ref=x["v_ref"],
-                                       ref_mass=False).o_tgt.float()
-                diff = (c.o_tgt[b].float() - fresh).flatten(2).norm(dim=-1)
-                errs.append((diff / (fresh.flatten(2).norm(dim=-1) + 1e-8)).flatten())
-
-        _timed_run(w, device, theta, delta_max=dmax, keep=keep)
-        e = torch.cat(errs).cpu()
-        cells.append({
-            "theta_q": tq, "theta_m": tm, "theta": theta, "delta_max": dmax,
-            "reuse_fraction": round(float((after0 == REUSE).float().mean()), 4),
-            "reuse_or_reactivate_fraction": round(float((after0 != COMPUTE).float().mean()), 4),
-            "attn_path_ms": round(sum(ms), 3),
-            "speedup_vs_full_fresh": round(full_ms / sum(ms), 3),
-            "boundary_block_per_step": [next((i for i, x in enumerate(row) if x == REACTIVATE), None)
-                                        for row in dec.tolist()],
-            "decisions": dec.tolist(),
-            "impact_mean": round(float(e.mean()), 5),
-            "impact_p99": round(float(e.quantile(0.99)), 5),
-            "impact_max": round(float(e.max()), 5),
-        })
+        c = _cell(w, device, full_ms, tq * tm, delta_max=dmax)
+        c.update(theta_q=tq, theta_m=tm)
+        cells.append(c)
         if log:
-            log(f"sweep: cell theta_q={tq} theta_m={tm} delta_max={dmax}: {cells[-1]['attn_path_ms']} ms, "
-                f"speedup {cells[-1]['speedup_vs_full_fresh']}, reuse {cells[-1]['reuse_fraction']}")
+            log(f"sweep: cell theta_q={tq} theta_m={tm} delta_max={dmax}: {c['attn_path_ms']} ms, "
+                f"speedup {c['speedup_vs_full_fresh']}, reuse {c['reuse_fraction']}")
+
+    # Cue ablation (the paper's ablation table, on these synthetics): each target-side or
+    # exposure cue alone, both with separate thresholds, the anchor-relative target-Q cue
+    # times exposure, and a fixed refresh every 3 steps.
+    ablation = []
+    if ablation_cells:
+        for tq, tm in ablation_cells:
+            for mode, theta, theta_m, cue in (("q_only", tq, None, "consecutive"),
+                                              ("mass_only", tm, None, "consecutive"),
+                                              ("and", tq, tm, "consecutive"),
+                                              ("product", tq * tm, None, "consecutive"),
+                                              ("product", tq * tm, None, "anchor")):
+                c = _cell(w, device, full_ms, theta, None, mode, theta_m, cue)
+                c.update(theta_q=tq, theta_m=tm)
+                c.pop("decisions")
+                ablation.append(c)
+                if log:
+                    log(f"sweep: ablation {mode}/{cue} theta_q={tq} theta_m={tm}: speedup "
+                        f"{c['speedup_vs_full_fresh']}, reuse {c['reuse_fraction']}, impact {c['impact_mean']}")
+        c = _cell(w, device, full_ms, math.inf, delta_max=3)
+        c.update(theta_q=None, theta_m=None, mode="fixed_interval_3")
+        c.pop("decisions")
+        ablation.append(c)
+        if log:
+            log(f"sweep: ablation fixed refresh every 3 steps: speedup {c['speedup_vs_full_fresh']}, "
+                f"impact {c['impact_mean']}")
+
     # The same trajectories replayed from captured HIP graphs (one graph per step).
     g_base, g_base_ms = _graph_timed_run(w, device, 0.0, delta_max=1)
     graph = {"full_fresh_attn_path_ms": round(sum(g_base_ms), 3), "cells": []}
@@ -263,6 +317,7 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2),
     for c in cells:
         c.pop("decisions")
     return {
+        "ablation": ablation,
         "graph_replay": graph,
         "workload": f"{w.n_blocks} blocks x {w.n_steps} steps, batch {w.batch}, {w.heads} heads, head_dim "
                     f"{w.head_dim}, n_ref {w.n_ref}, n_tgt {w.n_tgt}",

@@ -340,9 +340,12 @@ ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int
   if (n_ref == 0) return ok();
   ra_status s;
   if ((s = check_tensor("k_ref", k_ref, dtype, n_ref, head_dim)) != RA_OK) return s;
-  if ((s = check_tensor("v_ref", v_ref, dtype, n_ref, head_dim)) != RA_OK) return s;
   if ((s = check_tensor("k_cache", k_cache, dtype, n_ref, head_dim)) != RA_OK) return s;
-  if ((s = check_tensor("v_cache", v_cache, dtype, n_ref, head_dim)) != RA_OK) return s;
+  const bool k_only = v_ref.data == nullptr && v_cache.data == nullptr;
+  if (!k_only) {
+    if ((s = check_tensor("v_ref", v_ref, dtype, n_ref, head_dim)) != RA_OK) return s;
+    if ((s = check_tensor("v_cache", v_cache, dtype, n_ref, head_dim)) != RA_OK) return s;
+  }
   const hipError_t e = launch_cache_commit(dtype, batch, heads, n_ref, head_dim, view(k_ref), view(v_ref),
                                            view(k_cache), view(v_cache), decision, age, step,
                                            static_cast<hipStream_t>(stream));

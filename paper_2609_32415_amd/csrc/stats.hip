@@ -281,9 +281,11 @@ __global__ __launch_bounds__(CC_THREADS) void cache_commit_kernel(View ks, View 
     const int64_t do_k = ((b * kd.sb + h * kd.sh) + row * kd.ss + col) * esz;
     const int64_t do_v = ((b * vd.sb + h * vd.sh) + row * vd.ss + col) * esz;
     const u32x4 xk = *reinterpret_cast<const u32x4*>(static_cast<const char*>(ks.p) + so_k);
-    const u32x4 xv = *reinterpret_cast<const u32x4*>(static_cast<const char*>(vs.p) + so_v);
     *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(kd.p)) + do_k) = xk;
-    *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(vd.p)) + do_v) = xv;
+    if (vs.p != nullptr) {  // null V views: copy K only
+      const u32x4 xv = *reinterpret_cast<const u32x4*>(static_cast<const char*>(vs.p) + so_v);
+      *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(vd.p)) + do_v) = xv;
+    }
   }
   if (age && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *age = step;
 }

@@ -275,9 +275,12 @@ def q_change_gate(q_cur, q_prev, mass_prev, theta, state, block, step, mode="pro
 
 
 def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0):
-    """Copy fresh reference K/V into the cache when ``decision`` is COMPUTE (or None)."""
+    """Copy fresh reference K/V into the cache when ``decision`` is COMPUTE (or None);
+    with ``v_ref`` and ``v_cache`` None only K is copied."""
     B, H, n_ref, D = k_ref.shape
     dt = k_ref.dtype
+    if (v_ref is None) != (v_cache is None):
+        raise ValueError("v_ref and v_cache are both given or both None")
     for name, t in (("decision", decision), ("age", age)):
         _on_gpu(name, t)
         if t is not None and t.dtype != torch.int32:

@@ -36,18 +36,22 @@ def _x():
     return X
 
 
-def _margin_ok(tr, theta):
+def _margin_ok(tr, theta, mode="product", theta_m=None):
     th = np.broadcast_to(np.asarray(theta, dtype=np.float64), (W.n_blocks,))
-    mask = ~np.isnan(tr.g_mean)
-    return np.all(np.abs(tr.g_mean - th[None, :])[mask] > 1e-3)
+    score = {"product": tr.g_mean, "q_only": tr.d_mean, "mass_only": tr.m_mean, "and": tr.d_mean}[mode]
+    mask = ~np.isnan(score)
+    ok = np.all(np.abs(score - th[None, :])[mask] > 1e-3)
+    if mode == "and":
+        ok = ok and np.all(np.abs(tr.m_mean - theta_m)[~np.isnan(tr.m_mean)] > 1e-3)
+    return ok
 
 
-def _run_gpu(theta, delta_max=None, fused=True):
+def _run_gpu(theta, delta_max=None, fused=True, mode="product", theta_m=None, cue="consecutive"):
     from paper_2609_32415_amd.controller import Controller
 
     x = _x()
     ctl = Controller(W.n_blocks, W.n_steps, W.batch, W.heads, W.n_ref, W.n_tgt, W.head_dim, theta,
-                     delta_max=delta_max, device="cuda:0", fused=fused)
+                     delta_max=delta_max, device="cuda:0", fused=fused, mode=mode, theta_m=theta_m, cue=cue)
     outs, masses, ages = {}, {}, []
     for t in range(W.n_steps):
         xs = [{k: dev(v, "bf16") for k, v in x[(t, b)].items()} for b in range(W.n_blocks)]
@@ -74,6 +78,35 @@ def test_controller_matches_oracle(theta, delta_max, fused):
     if not _margin_ok(ref, theta):
         pytest.skip("a head-mean score lies within 1e-3 of theta for this seed")
     dec, outs, masses, ages = _run_gpu(theta, delta_max, fused)
+    assert dec.tolist() == ref.decisions.tolist()
+    assert ages.tolist() == ref.ages.tolist()
+    for (t, b), o in outs.items():
+        assert max_abs(o, ref.outputs[(t, b)]["o_tgt"]) <= O_TOL["bf16"], (t, b)
+        assert max_abs(masses[(t, b)], ref.outputs[(t, b)]["ref_mass"]) <= MASS_TOL["bf16"], (t, b)
+
+
+# (theta, delta_max, gate mode, theta_m, target-side cue): the single-cue ablations, the
+# two-threshold gate and the anchor-relative cue of the paper's ablation table.
+VARIANTS = [
+    (0.1, None, "q_only", None, "consecutive"),
+    (0.3, None, "mass_only", None, "consecutive"),
+    (0.2, None, "and", 0.4, "consecutive"),
+    (0.105, None, "product", None, "anchor"),
+    (0.115, 2, "product", None, "anchor"),
+    (1e9, 3, "product", None, "consecutive"),  # fixed-interval refresh (every 3 steps)
+]
+
+
+@pytest.mark.parametrize("theta,delta_max,mode,theta_m,cue", VARIANTS, ids=lambda v: str(v))
+def test_controller_variants_match_oracle(theta, delta_max, mode, theta_m, cue):
+    print(f"controller variant theta={theta} delta_max={delta_max} mode={mode} theta_m={theta_m} cue={cue}",
+          flush=True)
+    x = _x()
+    ref = run_controller(lambda t, b: x[(t, b)], W.n_steps, W.n_blocks, theta, delta_max=delta_max, mode=mode,
+                         theta_m=theta_m, cue=cue, keep_outputs=True)
+    if not _margin_ok(ref, theta, mode, theta_m):
+        pytest.skip("a head-mean score lies within 1e-3 of theta for this seed")
+    dec, outs, masses, ages = _run_gpu(theta, delta_max, True, mode, theta_m, cue)
     assert dec.tolist() == ref.decisions.tolist()
     assert ages.tolist() == ref.ages.tolist()
     for (t, b), o in outs.items():

@@ -180,6 +180,17 @@ def test_gate_thresholds_zero_and_infinite():
     assert int(dec.item()) == COMPUTE
 
 
+@pytest.mark.parametrize("decision,copied", [(2, True), (0, False)])
+def test_cache_commit_k_only(decision, copied):
+    """With both V views omitted only K is copied (the anchor-Q commit)."""
+    src = torch.randn((1, 3, 77, 128), device="cuda:0").to(torch.bfloat16)
+    dst = torch.zeros_like(src)
+    dec = torch.tensor([decision], dtype=torch.int32, device="cuda:0")
+    ops.cache_commit(src, None, dst, None, decision=dec)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src) if copied else bool((dst == 0).all())
+
+
 @pytest.mark.parametrize("decision,copied", [(2, True), (1, False), (0, False), (None, True)])
 def test_cache_commit(decision, copied):
     rng = np.random.default_rng(3)
