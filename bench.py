@@ -18,9 +18,10 @@ kernel (the full-fresh attention) measured live with HIP events on the launch
 stream, and the fp64 CPU oracle timed on a bounded sample of the same work.
 
 ``--sweep`` additionally runs the 60-block x 8-step controller sweep
-(single-reference shapes, 3 x 3 thresholds) and reports the reuse fraction,
-the attention-time speedup of adaptive reuse and the output error against a
-full-fresh trajectory.
+(single-reference shapes, 3 x 3 thresholds, cue ablation, graph replays) and
+reports the reuse fraction, the attention-time speedup of adaptive reuse and
+the output error against a full-fresh trajectory. ``--ref-sweep`` runs the
+reference-count sweep (1..8 reference images).
 """
 
 from __future__ import annotations
@@ -57,6 +58,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target duration of the oracle sample")
     ap.add_argument("--sweep", action="store_true", help="also run the 60-block x 8-step controller sweep")
+    ap.add_argument("--ref-sweep", action="store_true",
+                    help="also run the reference-count sweep (1..8 reference images at single-reference shapes)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the cache-commit copy over 2 x 512 MiB (a plain copy of known size, "
                     "for scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -297,6 +300,10 @@ def main():
         from paper_2609_32415_amd.controller import run_sweep
 
         out["sweep"] = run_sweep(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+    if args.ref_sweep:
+        from paper_2609_32415_amd.controller import run_ref_count_sweep
+
+        out["ref_count_sweep"] = run_ref_count_sweep(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
     print(json.dumps(out), flush=True)
 
 

@@ -325,3 +325,64 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2),
         "max_speedup_bound": round(w.n_steps / (1 + (w.n_steps - 1) * w.n_tgt / (w.n_ref + w.n_tgt)), 3),
         "cells": cells,
     }
+
+
+def run_ref_count_sweep(device="cuda:0", counts=(1, 2, 3, 4, 5, 6, 7, 8), n_blocks=8, theta_q=0.2, theta_m=0.4,
+                        log=None):
+    """Attention-time speedup against the number of reference images.
+
+    For k reference images of 4096 tokens plus 256 text tokens (N_R = 4096 k + 256,
+    N_Y = 4096, single-reference per-image shapes): the per-block attention times of a
+    computed block (all queries, fresh K/V) and a reused block (target queries, cached
+    K/V); the all-reuse bound of an n_steps trajectory, n t_full / (t_full + (n - 1)
+    t_reuse); and a measured controller trajectory (n_blocks blocks x 8 steps, sweep
+    recipe, product gate at theta_q * theta_m) against its full-fresh trajectory.
+    """
+    rows = []
+    for k in counts:
+        w = synth.workload("sweep", n_ref=4096 * k + 256, n_blocks=n_blocks)
+        tr = synth.DeviceTrajectory(w, 0, device)
+        tr.step_tensors(0)
+        x = tr.step_tensors(1)
+        del tr
+        ws_r = ops.attn_workspace(x["q_tgt"], w.n_ref, "target", "cache")
+        ws_f = ops.attn_workspace(x["q_tgt"], w.n_ref, "all", "fresh")
+
+        def timed(fn, n=10):
+            for _ in range(2):
+                fn()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(n):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / n
+
+        t_reuse = timed(lambda: ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_cache=x["k_ref"],
+                                               v_cache=x["v_ref"], n_ref=w.n_ref, kvsrc="cache", workspace=ws_r))
+        t_full = timed(lambda: ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"],
+                                              v_ref=x["v_ref"], qset="all", workspace=ws_f))
+        del x, ws_r, ws_f
+        _, base_ms = _timed_run(w, device, 0.0, delta_max=1)
+        ctl, ms = _timed_run(w, device, theta_q * theta_m, delta_max=None)
+        after0 = ctl.decisions.cpu()[1:]
+        n = w.n_steps
+        rows.append({
+            "ref_images": k, "n_ref": w.n_ref, "n_tgt": w.n_tgt,
+            "full_block_ms": round(t_full, 4), "reuse_block_ms": round(t_reuse, 4),
+            "block_speedup": round(t_full / t_reuse, 3),
+            "all_reuse_bound": round(n * t_full / (t_full + (n - 1) * t_reuse), 3),
+            "trajectory_full_fresh_ms": round(sum(base_ms), 3), "trajectory_adaptive_ms": round(sum(ms), 3),
+            "trajectory_speedup": round(sum(base_ms) / sum(ms), 3),
+            "reuse_fraction": round(float((after0 == REUSE).float().mean()), 4),
+        })
+        if log:
+            log(f"ref-count sweep: {k} references: block {rows[-1]['block_speedup']}x, trajectory "
+                f"{rows[-1]['trajectory_speedup']}x (reuse {rows[-1]['reuse_fraction']})")
+        torch.cuda.empty_cache()
+    return {"workload": f"{n_blocks} blocks x 8 steps, batch 1, 24 heads, head_dim 128, N_R = 4096 k + 256, "
+                        f"N_Y 4096; product gate at theta_q {theta_q} x theta_m {theta_m}",
+            "rows": rows}
+

@@ -240,14 +240,18 @@ def test_custom_scale_and_strided_views():
 
 
 FULL = [("single_ref", "target", "cache"), ("single_ref", "all", "fresh"), ("multi_ref", "target", "cache"),
-        ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"), ("video", "target", "cache")]
+        ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"), ("video", "target", "cache"),
+        ("ref8", "target", "cache"), ("ref8", "all", "fresh")]
 _FULL_CACHE = {}
+# eight 4096-token reference images plus 256 text tokens (the largest reference count swept)
+_NAMED = {"ref8": ("single_ref", {"n_ref": 8 * 4096 + 256})}
 
 
 def _full_inputs(name):
     if name not in _FULL_CACHE:
         _FULL_CACHE.clear()
-        w = synth.workload(name)
+        base, over = _NAMED.get(name, (name, {}))
+        w = synth.workload(base, **over)
         x = synth.block_inputs(w)
         x.update({f"{k}_cache": v for k, v in synth.stale_cache(w, x).items()})
         _FULL_CACHE[name] = (w, x)
