@@ -27,6 +27,12 @@ run_controller       Alg. 1 (monotone depth-adaptive reference reuse) as a
                      step/block loop over exogenous synthetic inputs.
 local_impact         Sec. 3.3 local-impact equation (relative Frobenius
                      change of the target attention output).
+diagnostics          The analysis quantities of Secs. 3.1-3.3 and App. A.2:
+                     consecutive and endpoint drift of K/V, the joint K/V
+                     endpoint scalar, the matched drift log-ratio, per-head
+                     exposure (fresh or with anchor reference keys), the
+                     reference-query mass on target keys and the adjacent
+                     reference-mass change.
 
 Every function is pinned by ``-m "not gpu"`` tests in ``tests/`` against
 closed forms, library routines (torch SDPA in fp64, scipy logsumexp),
@@ -37,6 +43,7 @@ the paper.
 from .joint_attention import joint_attention, joint_attention_loops
 from .stats import q_change, head_exposure, gate, GateResult, REUSE, REACTIVATE, COMPUTE
 from .controller import run_controller, local_impact, ControllerTrace
+from . import diagnostics
 
 __all__ = [
     "joint_attention",
@@ -51,4 +58,5 @@ __all__ = [
     "run_controller",
     "local_impact",
     "ControllerTrace",
+    "diagnostics",
 ]
