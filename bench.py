@@ -58,6 +58,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target duration of the oracle sample")
     ap.add_argument("--sweep", action="store_true", help="also run the 60-block x 8-step controller sweep")
+    ap.add_argument("--diagnostics", action="store_true",
+                    help="also run the diagnostics sidecar over a 60-block x 8-step controller trajectory")
     ap.add_argument("--ref-sweep", action="store_true",
                     help="also run the reference-count sweep (1..8 reference images at single-reference shapes)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -239,6 +241,21 @@ def main():
     ms["gate"] = timed(lambda: ops.gate(d_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec,
                                         score_out=score))
 
+    # Diagnostics sidecar kernels (read-only probes), at the same shapes.
+    ws_kv = ops.kv_drift_workspace(t["k_ref"])
+    ws_ratio = ops.drift_log_ratio_workspace(t["k_ref"], t["k_tgt"])
+    ws_imp = ops.output_impact_workspace(o_tgt_r)
+    diag_out = torch.empty((3, B, H), dtype=torch.float32, device=dev)
+    ms["kv_drift"] = timed(lambda: ops.kv_drift(t["k_ref"], cache_k, t["v_ref"], cache_v, d_k=diag_out[0],
+                                                d_v=diag_out[1], e_kv=diag_out[2], workspace=ws_kv))
+    k_prev_tgt = bf(x0["k_tgt"])
+    ms["ratio"] = timed(lambda: ops.drift_log_ratio(t["k_ref"], cache_k, t["k_tgt"], k_prev_tgt, d_ref=diag_out[0],
+                                                    d_tgt=diag_out[1], rho=diag_out[2], workspace=ws_ratio))
+    ms["impact"] = timed(lambda: ops.output_impact(o_tgt_r, o_tgt_f, out=diag_out[0], workspace=ws_imp))
+    ms["mass_mean"] = timed(lambda: ops.mass_mean(mass_f, out=diag_out[0]))
+    diag_bytes = {"kv_drift": 4 * B * H * n_ref * D * 2, "ratio": 2 * B * H * (n_ref + n_tgt) * D * 2,
+                  "impact": 2 * B * H * n_tgt * D * 2, "mass_mean": B * H * n_tgt * 4}
+
     f_reuse = attn_flops(H, n_tgt, n_ref + n_tgt, D, B)
     f_full = attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, D, B)
     value = (f_reuse + f_full) / (ms_per_step * 1e-3) / 1e12
@@ -282,6 +299,13 @@ def main():
             "gate_us": round(ms["gate"] * 1e3, 2),
             "gate_gbs": round((B * H * n_tgt * 4 + B * H * 4) / (ms["gate"] * 1e-3) / 1e9, 1),
             "commit_us": round(ms["commit"] * 1e3, 2),
+            "diag_kv_drift_us": round(ms["kv_drift"] * 1e3, 2),
+            "diag_kv_drift_gbs": round(diag_bytes["kv_drift"] / (ms["kv_drift"] * 1e-3) / 1e9, 1),
+            "diag_drift_log_ratio_us": round(ms["ratio"] * 1e3, 2),
+            "diag_drift_log_ratio_gbs": round(diag_bytes["ratio"] / (ms["ratio"] * 1e-3) / 1e9, 1),
+            "diag_output_impact_us": round(ms["impact"] * 1e3, 2),
+            "diag_output_impact_gbs": round(diag_bytes["impact"] / (ms["impact"] * 1e-3) / 1e9, 1),
+            "diag_mass_mean_us": round(ms["mass_mean"] * 1e3, 2),
         },
         "roofline": {
             "kernel": "attn_bf16_kernel<128> (full-fresh mode, with the key-split merge of its last round)",
@@ -300,6 +324,10 @@ def main():
         from paper_2609_32415_amd.controller import run_sweep
 
         out["sweep"] = run_sweep(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+    if args.diagnostics:
+        from paper_2609_32415_amd.controller import run_diagnostics
+
+        out["diagnostics"] = run_diagnostics(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
     if args.ref_sweep:
         from paper_2609_32415_amd.controller import run_ref_count_sweep
 

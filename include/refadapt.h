@@ -243,6 +243,103 @@ ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int
                                 ra_tensor k_ref, ra_tensor v_ref, ra_tensor k_cache, ra_tensor v_cache,
                                 const int32_t* decision, int32_t* age, int32_t step, void* stream);
 
+/* ---- Diagnostics sidecar --------------------------------------------------
+ *
+ * Read-only probes of the controlled path (paper App. "probe non-intrusiveness":
+ * enabling them leaves every output of the path bitwise unchanged). Each call
+ * reads its inputs, writes only its own outputs and workspace, and enqueues on
+ * `stream` without synchronising. Sums are fp32 within a workgroup and fp64
+ * across workgroups and for the final ratios, in a fixed order, so results are
+ * bitwise reproducible. Tensors follow the ra_tensor rules of refadapt_q_change
+ * (16-byte aligned base, strides in whole 16-byte units, d contiguous).
+ * Workspaces need no initialisation and must be 8-byte aligned.
+ */
+
+/*
+ * refadapt_kv_drift - relative change of a reference K/V pair against a base.
+ *
+ *   d_k[b, h]  = ||K_cur[b,h] - K_base[b,h]||_F / (||K_base[b,h]||_F + eps)
+ *   d_v[b, h]  = the same for V
+ *   e_kv[b, h] = (d_k[b, h] + d_v[b, h]) / 2
+ * over the n_rows x head_dim slice of each (b, h). With K_base/V_base the
+ * cached (anchor) reference K/V this is the endpoint drift D_{t|a} of Sec. 3.3
+ * (endpoint-drift equation) and e_kv its joint K/V scalar E^KV (the mean of the
+ * two head-resolved drifts); with the previous step's K/V it is the consecutive
+ * drift of Sec. 3.1. d_k and d_v may be NULL; e_kv is required. Outputs are
+ * [B, H] contiguous fp32. One launch pair covers both tensors.
+ * Errors: RA_EINVAL (sizes, dtype, eps, null tensors or e_kv), RA_EUNSUPPORTED
+ * (head_dim, alignment), RA_EWORKSPACE (workspace NULL or smaller than
+ * refadapt_kv_drift_workspace_size).
+ */
+size_t refadapt_kv_drift_workspace_size(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim);
+ra_status refadapt_kv_drift(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
+                            ra_tensor k_cur, ra_tensor k_base, ra_tensor v_cur, ra_tensor v_base, float eps,
+                            float* d_k, float* d_v, float* e_kv, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * refadapt_drift_log_ratio - matched reference/target drift log-ratio.
+ *
+ *   d_ref[b, h] = ||Z_ref_cur - Z_ref_prev||_F / (||Z_ref_prev||_F + eps)   (n_ref rows)
+ *   d_tgt[b, h] = ||Z_tgt_cur - Z_tgt_prev||_F / (||Z_tgt_prev||_F + eps)   (n_tgt rows)
+ *   rho[b, h]   = log10((d_ref + eps) / (d_tgt + eps))
+ * for one tensor Z of K or V at adjacent steps (Sec. 3.1 consecutive-drift and
+ * drift-log-ratio equations): rho < 0 means the reference slice moves more
+ * slowly than the target slice. d_ref and d_tgt may be NULL; rho is required.
+ * With eps == 0 a zero drift gives an infinite or NaN rho (IEEE division).
+ * Errors: as refadapt_kv_drift, with refadapt_drift_log_ratio_workspace_size.
+ */
+size_t refadapt_drift_log_ratio_workspace_size(int32_t batch, int32_t heads, int32_t n_ref, int32_t n_tgt,
+                                               int32_t head_dim);
+ra_status refadapt_drift_log_ratio(int32_t batch, int32_t heads, int32_t n_ref, int32_t n_tgt, int32_t head_dim,
+                                   int32_t dtype, ra_tensor z_ref_cur, ra_tensor z_ref_prev, ra_tensor z_tgt_cur,
+                                   ra_tensor z_tgt_prev, float eps, float* d_ref, float* d_tgt, float* rho,
+                                   void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * refadapt_output_impact - local perturbation of a stale-K/V attention output.
+ *
+ *   impact[b, h] = ||O_stale[b,h] - O_fresh[b,h]||_F / (||O_fresh[b,h]||_F + eps)
+ * over the n_rows x head_dim slice (Sec. 3.3 local-impact equation, I^KV):
+ * O_stale is the target output over cached reference K/V (refadapt_joint_attn
+ * with RA_KV_CACHE, or the executed output of a reused block), O_fresh the
+ * target output over fresh K/V. Both outputs are read once, in one pass.
+ * impact is [B, H] contiguous fp32.
+ * Errors: as refadapt_kv_drift, with refadapt_output_impact_workspace_size.
+ */
+size_t refadapt_output_impact_workspace_size(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim);
+ra_status refadapt_output_impact(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
+                                 ra_tensor o_stale, ra_tensor o_fresh, float eps, float* impact, void* workspace,
+                                 size_t ws_bytes, void* stream);
+
+/*
+ * refadapt_mass_mean - head-resolved mean of per-query reference mass.
+ *
+ *   out[b, h] = mean over r < n_rows of mass[b, h, r]          (complement == 0)
+ *   out[b, h] = mean over r < n_rows of (1 - mass[b, h, r])    (complement == 1)
+ * with mass [B, H, n_rows] contiguous fp32 as written by refadapt_joint_attn.
+ * From ref_mass (target queries) this is the head exposure M_{t,b,h} of
+ * Sec. 3.2 (directional-exposure equation); from a REUSE launch's ref_mass it is
+ * the same-step cached exposure M^cached of App. A.2; complement = 1 over
+ * ref_mass_refq (reference queries) gives the reference-query mass on target
+ * keys (App. directional attention diagnostics). out is [B, H] fp32.
+ * Errors: RA_EINVAL (sizes, null pointers, complement not 0 or 1).
+ */
+ra_status refadapt_mass_mean(int32_t batch, int32_t heads, int32_t n_rows, const float* mass, int32_t complement,
+                             float* out, void* stream);
+
+/*
+ * refadapt_adjacent_mass_change - mean adjacent-step change of head-mean mass.
+ *
+ * With mass_mean [n_steps, n_blocks, bh] contiguous fp32 (per step and block,
+ * the bh values M_{t,b,(b',h)} of refadapt_mass_mean) and Mbar_{t,b} their mean
+ * over bh, writes per block
+ *   out[b] = 100 / (n_steps - 1) * sum_{t >= 1} |Mbar_{t,b} - Mbar_{t-1,b}|
+ * in percentage points (Sec. 3.2 adjacent-ref-change equation).
+ * Errors: RA_EINVAL (n_steps < 2, n_blocks or bh < 1, null pointers).
+ */
+ra_status refadapt_adjacent_mass_change(int32_t n_steps, int32_t n_blocks, int32_t bh, const float* mass_mean,
+                                        float* out, void* stream);
+
 /* Message describing the calling thread's last non-OK status ("" if none). */
 const char* refadapt_last_error(void);
 

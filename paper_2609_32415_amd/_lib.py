@@ -41,6 +41,14 @@ EXPORTED = (
     "refadapt_q_change_gate_workspace_size",
     "refadapt_q_change_gate",
     "refadapt_cache_commit",
+    "refadapt_kv_drift_workspace_size",
+    "refadapt_kv_drift",
+    "refadapt_drift_log_ratio_workspace_size",
+    "refadapt_drift_log_ratio",
+    "refadapt_output_impact_workspace_size",
+    "refadapt_output_impact",
+    "refadapt_mass_mean",
+    "refadapt_adjacent_mass_change",
     "refadapt_last_error",
     "refadapt_version",
 )
@@ -130,6 +138,25 @@ def _load():
     lib.refadapt_q_change_gate.restype = i32
     lib.refadapt_cache_commit.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor, ra_tensor, vp, vp, i32, vp]
     lib.refadapt_cache_commit.restype = i32
+    lib.refadapt_kv_drift_workspace_size.argtypes = [i32, i32, i32, i32]
+    lib.refadapt_kv_drift_workspace_size.restype = ctypes.c_size_t
+    lib.refadapt_kv_drift.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor, ra_tensor, f32,
+                                      vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.refadapt_kv_drift.restype = i32
+    lib.refadapt_drift_log_ratio_workspace_size.argtypes = [i32, i32, i32, i32, i32]
+    lib.refadapt_drift_log_ratio_workspace_size.restype = ctypes.c_size_t
+    lib.refadapt_drift_log_ratio.argtypes = [i32, i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor,
+                                             ra_tensor, f32, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.refadapt_drift_log_ratio.restype = i32
+    lib.refadapt_output_impact_workspace_size.argtypes = [i32, i32, i32, i32]
+    lib.refadapt_output_impact_workspace_size.restype = ctypes.c_size_t
+    lib.refadapt_output_impact.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, vp, vp,
+                                           ctypes.c_size_t, vp]
+    lib.refadapt_output_impact.restype = i32
+    lib.refadapt_mass_mean.argtypes = [i32, i32, i32, vp, i32, vp, vp]
+    lib.refadapt_mass_mean.restype = i32
+    lib.refadapt_adjacent_mass_change.argtypes = [i32, i32, i32, vp, vp, vp]
+    lib.refadapt_adjacent_mass_change.restype = i32
     lib.refadapt_last_error.argtypes = []
     lib.refadapt_last_error.restype = ctypes.c_char_p
     lib.refadapt_version.argtypes = []
@@ -180,6 +207,45 @@ def refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, 
 
 def refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, k_cache, v_cache, decision, age, step, stream):
     return _check(LIB.refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, k_cache, v_cache, decision, age, step, stream))
+
+
+def refadapt_kv_drift_workspace_size(batch, heads, n_rows, head_dim):
+    return int(LIB.refadapt_kv_drift_workspace_size(batch, heads, n_rows, head_dim))
+
+
+def refadapt_kv_drift(batch, heads, n_rows, head_dim, dtype, k_cur, k_base, v_cur, v_base, eps, d_k, d_v, e_kv,
+                      workspace, ws_bytes, stream):
+    return _check(LIB.refadapt_kv_drift(batch, heads, n_rows, head_dim, dtype, k_cur, k_base, v_cur, v_base, eps,
+                                        d_k, d_v, e_kv, workspace, ws_bytes, stream))
+
+
+def refadapt_drift_log_ratio_workspace_size(batch, heads, n_ref, n_tgt, head_dim):
+    return int(LIB.refadapt_drift_log_ratio_workspace_size(batch, heads, n_ref, n_tgt, head_dim))
+
+
+def refadapt_drift_log_ratio(batch, heads, n_ref, n_tgt, head_dim, dtype, z_ref_cur, z_ref_prev, z_tgt_cur,
+                             z_tgt_prev, eps, d_ref, d_tgt, rho, workspace, ws_bytes, stream):
+    return _check(LIB.refadapt_drift_log_ratio(batch, heads, n_ref, n_tgt, head_dim, dtype, z_ref_cur, z_ref_prev,
+                                               z_tgt_cur, z_tgt_prev, eps, d_ref, d_tgt, rho, workspace, ws_bytes,
+                                               stream))
+
+
+def refadapt_output_impact_workspace_size(batch, heads, n_rows, head_dim):
+    return int(LIB.refadapt_output_impact_workspace_size(batch, heads, n_rows, head_dim))
+
+
+def refadapt_output_impact(batch, heads, n_rows, head_dim, dtype, o_stale, o_fresh, eps, impact, workspace,
+                           ws_bytes, stream):
+    return _check(LIB.refadapt_output_impact(batch, heads, n_rows, head_dim, dtype, o_stale, o_fresh, eps, impact,
+                                             workspace, ws_bytes, stream))
+
+
+def refadapt_mass_mean(batch, heads, n_rows, mass, complement, out, stream):
+    return _check(LIB.refadapt_mass_mean(batch, heads, n_rows, mass, complement, out, stream))
+
+
+def refadapt_adjacent_mass_change(n_steps, n_blocks, bh, mass_mean, out, stream):
+    return _check(LIB.refadapt_adjacent_mass_change(n_steps, n_blocks, bh, mass_mean, out, stream))
 
 
 def refadapt_last_error():

@@ -44,7 +44,7 @@ class Controller:
 
     def __init__(self, n_blocks, n_steps, batch, heads, n_ref, n_tgt, head_dim, theta, delta_max=None,
                  mode="product", theta_m=None, dtype=torch.bfloat16, device="cuda:0", eps=1e-8, fused=True,
-                 cue="consecutive"):
+                 cue="consecutive", sidecar=None):
         self.nb, self.n_steps = n_blocks, n_steps
         self.shape_r = (batch, heads, n_ref, head_dim)
         self.shape_t = (batch, heads, n_tgt, head_dim)
@@ -79,6 +79,7 @@ class Controller:
         self.fused = fused
         self.ws = ops.q_change_gate_workspace(q_like) if fused else ops.q_change_workspace(q_like)
         self.attn_ws = ops.attn_workspace(q_like, n_ref, kvsrc="device")
+        self.sidecar = sidecar
 
     def block(self, t, b, x):
         """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``."""
@@ -101,6 +102,8 @@ class Controller:
             k_cache=self.k_cache[b], v_cache=self.v_cache[b], kvsrc="device", decision=dec,
             o_tgt=self.o_tgt[b], o_ref=self.o_ref[b], ref_mass=self.mass[b][nxt], workspace=self.attn_ws,
         )
+        if self.sidecar is not None:  # read-only probes; the block's cache still holds its anchor K/V
+            self.sidecar.block(t, b, x, self)
         ops.cache_commit(x["k_ref"], x["v_ref"], self.k_cache[b], self.v_cache[b], decision=dec,
                          age=self.age[b:b + 1], step=t)
         if self.cue == "anchor":
@@ -116,6 +119,83 @@ class Controller:
     def recorded_mass(self, b):
         """Per-query reference mass of block b's most recently executed attention."""
         return self.mass[b][self.parity[b]]
+
+
+class Sidecar:
+    """Diagnostics sidecar of one controller trajectory: read-only probes per block and step.
+
+    Called by ``Controller.block`` after the block's attention and before its cache
+    commit, so the block's cache still holds the reference K/V of its last COMPUTE
+    step (the anchor a_b). Everything is enqueued on the current stream into the
+    sidecar's own buffers and device logs ``[n_steps, n_blocks, B, H]`` (NaN where
+    a quantity is undefined, e.g. drifts at step 0); nothing the controller reads
+    or writes is touched, so its outputs are bitwise the same with or without it.
+
+    Logged per (t, b, batch, head):
+      e_kv, d_k, d_v  endpoint drift of the fresh reference K and V against the
+                      cached anchor values and their mean E^KV (t >= 1)
+      rho_k, rho_v    matched log-ratio of reference vs target consecutive drift
+                      of K and of V (t >= 1)
+      impact          I^KV of the executed target output against the full-fresh
+                      target output of the same step
+      m_fresh         exposure of the current target queries over fresh keys
+      m_cached        same-step exposure with the cached (anchor) reference keys
+                      (t >= 1)
+      m_refq_tgt      mean mass of the reference queries on target keys
+    ``adjacent_change()`` gives the per-block adjacent reference-mass change (in
+    percentage points) of the logged fresh exposure.
+    """
+
+    def __init__(self, n_blocks, n_steps, batch, heads, n_ref, n_tgt, head_dim, dtype=torch.bfloat16,
+                 device="cuda:0", eps=1e-8):
+        self.eps = eps
+        shape = (n_steps, n_blocks, batch, heads)
+        nan = lambda: torch.full(shape, float("nan"), dtype=torch.float32, device=device)
+        self.e_kv, self.d_k, self.d_v = nan(), nan(), nan()
+        self.rho_k, self.rho_v = nan(), nan()
+        self.impact, self.m_fresh, self.m_cached, self.m_refq_tgt = nan(), nan(), nan(), nan()
+        sr, st = (batch, heads, n_ref, head_dim), (batch, heads, n_tgt, head_dim)
+        self.o_fresh = torch.empty(st, dtype=dtype, device=device)
+        self.o_ref_fresh = torch.empty(sr, dtype=dtype, device=device)
+        self.o_cached = torch.empty(st, dtype=dtype, device=device)
+        self.mass_fresh = torch.empty((batch, heads, n_tgt), dtype=torch.float32, device=device)
+        self.mass_refq = torch.empty((batch, heads, n_ref), dtype=torch.float32, device=device)
+        self.mass_cached = torch.empty((batch, heads, n_tgt), dtype=torch.float32, device=device)
+        q_like = torch.empty(st, dtype=dtype, device=device)
+        r_like = torch.empty(sr, dtype=dtype, device=device)
+        self.ws_full = ops.attn_workspace(q_like, n_ref, qset="all", kvsrc="fresh")
+        self.ws_cached = ops.attn_workspace(q_like, n_ref, qset="target", kvsrc="cache")
+        self.ws_kv = ops.kv_drift_workspace(r_like)
+        self.ws_ratio = ops.drift_log_ratio_workspace(r_like, q_like)
+        self.ws_impact = ops.output_impact_workspace(q_like)
+        self.prev = [None] * n_blocks
+
+    def block(self, t, b, x, ctl):
+        eps = self.eps
+        # Full-fresh joint attention of the step: target and reference queries over fresh K/V.
+        ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"], v_ref=x["v_ref"],
+                       qset="all", kvsrc="fresh", o_tgt=self.o_fresh, o_ref=self.o_ref_fresh,
+                       ref_mass=self.mass_fresh, ref_mass_refq=self.mass_refq, workspace=self.ws_full)
+        ops.mass_mean(self.mass_fresh, out=self.m_fresh[t, b])
+        ops.mass_mean(self.mass_refq, complement=True, out=self.m_refq_tgt[t, b])
+        ops.output_impact(ctl.o_tgt[b], self.o_fresh, eps, out=self.impact[t, b], workspace=self.ws_impact)
+        if t > 0:
+            ops.kv_drift(x["k_ref"], ctl.k_cache[b], x["v_ref"], ctl.v_cache[b], eps, d_k=self.d_k[t, b],
+                         d_v=self.d_v[t, b], e_kv=self.e_kv[t, b], workspace=self.ws_kv)
+            ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_cache=ctl.k_cache[b], v_cache=ctl.v_cache[b],
+                           qset="target", kvsrc="cache", o_tgt=self.o_cached, ref_mass=self.mass_cached,
+                           workspace=self.ws_cached)
+            ops.mass_mean(self.mass_cached, out=self.m_cached[t, b])
+            p = self.prev[b]
+            ops.drift_log_ratio(x["k_ref"], p["k_ref"], x["k_tgt"], p["k_tgt"], eps, rho=self.rho_k[t, b],
+                                workspace=self.ws_ratio)
+            ops.drift_log_ratio(x["v_ref"], p["v_ref"], x["v_tgt"], p["v_tgt"], eps, rho=self.rho_v[t, b],
+                                workspace=self.ws_ratio)
+        self.prev[b] = {k: x[k] for k in ("k_ref", "v_ref", "k_tgt", "v_tgt")}
+
+    def adjacent_change(self):
+        """Per-block adjacent reference-mass change (percentage points) of the fresh exposure."""
+        return ops.adjacent_mass_change(self.m_fresh)
 
 
 class StepGraphs:
@@ -165,10 +245,11 @@ def _sweep_inputs(w, device):
     return trajs
 
 
-def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=None, cue="consecutive"):
+def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=None, cue="consecutive",
+               sidecar=None):
     """One trajectory; returns (controller, per-step attention-path milliseconds)."""
     ctl = Controller(w.n_blocks, w.n_steps, w.batch, w.heads, w.n_ref, w.n_tgt, w.head_dim, theta,
-                     delta_max=delta_max, mode=mode, theta_m=theta_m, device=device, cue=cue)
+                     delta_max=delta_max, mode=mode, theta_m=theta_m, device=device, cue=cue, sidecar=sidecar)
     trajs = _sweep_inputs(w, device)
     step_ms = []
     for t in range(w.n_steps):
@@ -325,6 +406,93 @@ def run_sweep(device="cuda:0", w=None, log=None, delta_max_cells=((0.2, 0.4, 2),
         "max_speedup_bound": round(w.n_steps / (1 + (w.n_steps - 1) * w.n_tgt / (w.n_ref + w.n_tgt)), 3),
         "cells": cells,
     }
+
+
+def _ranks(a):
+    """Ranks (average ranks for ties) of a 1-D array, for Spearman's correlation."""
+    import numpy as np
+
+    order = np.argsort(a, kind="stable")
+    r = np.empty(len(a), dtype=np.float64)
+    r[order] = np.arange(len(a), dtype=np.float64)
+    vals, inv, counts = np.unique(a, return_inverse=True, return_counts=True)
+    sums = np.bincount(inv, weights=r)
+    return (sums / counts)[inv]
+
+
+def run_diagnostics(device="cuda:0", w=None, theta=(0.1, 0.2), log=None):
+    """The diagnostics sidecar over one controller trajectory (sweep shapes, 60 blocks x 8 steps).
+
+    Runs the trajectory twice on the same inputs, without and with the sidecar,
+    and checks that every controller output and state tensor is bitwise the same
+    (the probe reads only). Summaries of the sidecar's device logs (steps >= 1
+    where a quantity needs an anchor or a previous step):
+      endpoint drift E^KV of the reference K/V against each block's anchor;
+      median of the matched drift log-ratio rho for K and V and the ratio 10^rho;
+      I^KV of the executed target output against full-fresh attention;
+      per-block adjacent reference-mass change (percentage points);
+      same-step cached vs fresh exposure: mean absolute difference, Pearson and
+      Spearman correlation over (step, block, head) cells;
+      mean mass of reference queries on target keys vs of target queries on
+      reference keys, and the share of (step, block) cells where the first is larger;
+      the sidecar's share of the attention-path time.
+    Correlation statistics are computed on the host from the logged arrays.
+    """
+    import numpy as np
+
+    w = w or synth.workload("sweep")
+    th = theta[0] * theta[1]
+    ctl_off, ms_off = _timed_run(w, device, th, None)
+    final_off = [x.clone() for x in ctl_off.o_tgt + ctl_off.o_ref + [m for p in ctl_off.mass for m in p]
+                 + ctl_off.k_cache + ctl_off.v_cache + [ctl_off.d, ctl_off.age, ctl_off.decisions, ctl_off.scores]]
+    del ctl_off
+    torch.cuda.empty_cache()
+    sc = Sidecar(w.n_blocks, w.n_steps, w.batch, w.heads, w.n_ref, w.n_tgt, w.head_dim, device=device)
+    ctl_on, ms_on = _timed_run(w, device, th, None, sidecar=sc)
+    final_on = ctl_on.o_tgt + ctl_on.o_ref + [m for p in ctl_on.mass for m in p] + ctl_on.k_cache + \
+        ctl_on.v_cache + [ctl_on.d, ctl_on.age, ctl_on.decisions, ctl_on.scores]
+    identical = all(torch.equal(a, b) for a, b in zip(final_off, final_on))
+    dbar = sc.adjacent_change()
+    torch.cuda.synchronize()
+    h = lambda x: x.cpu().numpy().astype(np.float64)
+    e_kv, rho_k, rho_v, imp = h(sc.e_kv)[1:], h(sc.rho_k)[1:], h(sc.rho_v)[1:], h(sc.impact)
+    m_f, m_c, m_q = h(sc.m_fresh), h(sc.m_cached)[1:], h(sc.m_refq_tgt)
+    dec = ctl_on.decisions.cpu().numpy()
+    reused = dec == REUSE
+    mf1 = m_f[1:].reshape(-1)
+    mc1 = m_c.reshape(-1)
+    pearson = float(np.corrcoef(mf1, mc1)[0, 1])
+    spearman = float(np.corrcoef(_ranks(mf1), _ranks(mc1))[0, 1])
+    cell_refq = m_q.mean(axis=(2, 3))  # [T, n_blocks] head means
+    cell_tgt = m_f.mean(axis=(2, 3))
+    res = {
+        "theta": list(theta),
+        "bit_identical_with_sidecar": bool(identical),
+        "attn_path_ms": round(sum(ms_off), 3),
+        "attn_path_with_sidecar_ms": round(sum(ms_on), 3),
+        "sidecar_share_of_path_time": round(sum(ms_on) / sum(ms_off) - 1.0, 3),
+        "endpoint_e_kv": {"mean": round(float(e_kv.mean()), 5), "median": round(float(np.median(e_kv)), 5),
+                          "max": round(float(e_kv.max()), 5)},
+        "rho_k_median": round(float(np.median(rho_k)), 4),
+        "rho_v_median": round(float(np.median(rho_v)), 4),
+        "ref_over_tgt_drift_median_k": round(float(10 ** np.median(rho_k)), 4),
+        "ref_over_tgt_drift_median_v": round(float(10 ** np.median(rho_v)), 4),
+        "impact_mean": round(float(imp.mean()), 5),
+        "impact_reused_blocks_mean": round(float(imp[reused].mean()), 5) if reused.any() else None,
+        "impact_p99": round(float(np.quantile(imp, 0.99)), 5),
+        "adjacent_ref_change_pp": {"max": round(float(h(dbar).max()), 4), "mean": round(float(h(dbar).mean()), 4)},
+        "cached_vs_fresh_exposure": {"mad": round(float(np.abs(mf1 - mc1).mean()), 6),
+                                     "pearson": round(pearson, 5), "spearman": round(spearman, 5)},
+        "target_to_ref_mass_mean": round(float(m_f.mean()), 5),
+        "ref_query_to_target_mass_mean": round(float(m_q.mean()), 5),
+        "refq_gt_tgt_cell_share": round(float((cell_refq > cell_tgt).mean()), 4),
+        "reuse_fraction": round(float(reused[1:].mean()), 4),
+    }
+    if log:
+        log(f"diagnostics: bit-identical {identical}, sidecar +{100 * res['sidecar_share_of_path_time']:.0f}% of "
+            f"path time, median 10^rho K {res['ref_over_tgt_drift_median_k']} V {res['ref_over_tgt_drift_median_v']}, "
+            f"cached-vs-fresh MAD {res['cached_vs_fresh_exposure']['mad']}")
+    return res
 
 
 def run_ref_count_sweep(device="cuda:0", counts=(1, 2, 3, 4, 5, 6, 7, 8), n_blocks=8, theta_q=0.2, theta_m=0.4,

@@ -353,3 +353,144 @@ ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int
 }
 
 }  // extern "C"
+
+// ---- diagnostics sidecar
+
+namespace {
+
+ra_status check_pair_common(const char* fn, int32_t batch, int32_t heads, int32_t head_dim, int32_t dtype,
+                            float eps) {
+  if (batch < 1 || heads < 1) return fail(RA_EINVAL, "%s: batch and heads must be >= 1", fn);
+  if (dtype != RA_BF16 && dtype != RA_F32) return fail(RA_EINVAL, "%s: unknown dtype %d", fn, dtype);
+  if (head_dim < 1 || head_dim % (dtype == RA_BF16 ? 8 : 4) != 0)
+    return fail(RA_EUNSUPPORTED, "%s: head_dim %d must be a positive multiple of %d", fn, head_dim,
+                dtype == RA_BF16 ? 8 : 4);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RA_EINVAL, "%s: eps must be finite and >= 0", fn);
+  return RA_OK;
+}
+
+ra_status check_workspace(const char* fn, void* ws, size_t ws_bytes, size_t need) {
+  if (ws == nullptr || ws_bytes < need)
+    return fail(RA_EWORKSPACE, "%s: workspace needs %zu bytes (got %zu)", fn, need, ws ? ws_bytes : 0);
+  if ((reinterpret_cast<uintptr_t>(ws) & 7) != 0) return fail(RA_EUNSUPPORTED, "%s: workspace must be 8-byte aligned", fn);
+  return RA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t refadapt_kv_drift_workspace_size(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim) {
+  if (batch < 1 || heads < 1 || n_rows < 1 || head_dim < 1) return 0;
+  const int32_t rows[2] = {n_rows, n_rows};
+  return pair_workspace_bytes(batch, heads, head_dim, 2, rows);
+}
+
+ra_status refadapt_kv_drift(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
+                            ra_tensor k_cur, ra_tensor k_base, ra_tensor v_cur, ra_tensor v_base, float eps,
+                            float* d_k, float* d_v, float* e_kv, void* workspace, size_t ws_bytes, void* stream) {
+  ra_status s;
+  if ((s = check_pair_common("kv_drift", batch, heads, head_dim, dtype, eps)) != RA_OK) return s;
+  if (n_rows < 1) return fail(RA_EINVAL, "kv_drift: n_rows must be >= 1");
+  if ((s = check_tensor("k_cur", k_cur, dtype, n_rows, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("k_base", k_base, dtype, n_rows, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("v_cur", v_cur, dtype, n_rows, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("v_base", v_base, dtype, n_rows, head_dim)) != RA_OK) return s;
+  if (e_kv == nullptr) return fail(RA_EINVAL, "kv_drift: null e_kv");
+  if ((s = check_workspace("kv_drift", workspace, ws_bytes,
+                           refadapt_kv_drift_workspace_size(batch, heads, n_rows, head_dim))) != RA_OK)
+    return s;
+  PairSet ps{};
+  ps.cur[0] = view(k_cur);
+  ps.base[0] = view(k_base);
+  ps.cur[1] = view(v_cur);
+  ps.base[1] = view(v_base);
+  ps.n_rows[0] = ps.n_rows[1] = n_rows;
+  const hipError_t e = launch_pair_change(dtype, batch, heads, head_dim, 2, ps, PAIR_KV, eps, d_k, d_v, e_kv,
+                                          workspace, static_cast<hipStream_t>(stream));
+  return launch_status(e, "kv_drift");
+}
+
+size_t refadapt_drift_log_ratio_workspace_size(int32_t batch, int32_t heads, int32_t n_ref, int32_t n_tgt,
+                                               int32_t head_dim) {
+  if (batch < 1 || heads < 1 || n_ref < 1 || n_tgt < 1 || head_dim < 1) return 0;
+  const int32_t rows[2] = {n_ref, n_tgt};
+  return pair_workspace_bytes(batch, heads, head_dim, 2, rows);
+}
+
+ra_status refadapt_drift_log_ratio(int32_t batch, int32_t heads, int32_t n_ref, int32_t n_tgt, int32_t head_dim,
+                                   int32_t dtype, ra_tensor z_ref_cur, ra_tensor z_ref_prev, ra_tensor z_tgt_cur,
+                                   ra_tensor z_tgt_prev, float eps, float* d_ref, float* d_tgt, float* rho,
+                                   void* workspace, size_t ws_bytes, void* stream) {
+  ra_status s;
+  if ((s = check_pair_common("drift_log_ratio", batch, heads, head_dim, dtype, eps)) != RA_OK) return s;
+  if (n_ref < 1 || n_tgt < 1) return fail(RA_EINVAL, "drift_log_ratio: n_ref and n_tgt must be >= 1");
+  if ((s = check_tensor("z_ref_cur", z_ref_cur, dtype, n_ref, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("z_ref_prev", z_ref_prev, dtype, n_ref, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("z_tgt_cur", z_tgt_cur, dtype, n_tgt, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("z_tgt_prev", z_tgt_prev, dtype, n_tgt, head_dim)) != RA_OK) return s;
+  if (rho == nullptr) return fail(RA_EINVAL, "drift_log_ratio: null rho");
+  if ((s = check_workspace("drift_log_ratio", workspace, ws_bytes,
+                           refadapt_drift_log_ratio_workspace_size(batch, heads, n_ref, n_tgt, head_dim))) != RA_OK)
+    return s;
+  PairSet ps{};
+  ps.cur[0] = view(z_ref_cur);
+  ps.base[0] = view(z_ref_prev);
+  ps.cur[1] = view(z_tgt_cur);
+  ps.base[1] = view(z_tgt_prev);
+  ps.n_rows[0] = n_ref;
+  ps.n_rows[1] = n_tgt;
+  const hipError_t e = launch_pair_change(dtype, batch, heads, head_dim, 2, ps, PAIR_RATIO, eps, d_ref, d_tgt, rho,
+                                          workspace, static_cast<hipStream_t>(stream));
+  return launch_status(e, "drift_log_ratio");
+}
+
+size_t refadapt_output_impact_workspace_size(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim) {
+  if (batch < 1 || heads < 1 || n_rows < 1 || head_dim < 1) return 0;
+  return pair_workspace_bytes(batch, heads, head_dim, 1, &n_rows);
+}
+
+ra_status refadapt_output_impact(int32_t batch, int32_t heads, int32_t n_rows, int32_t head_dim, int32_t dtype,
+                                 ra_tensor o_stale, ra_tensor o_fresh, float eps, float* impact, void* workspace,
+                                 size_t ws_bytes, void* stream) {
+  ra_status s;
+  if ((s = check_pair_common("output_impact", batch, heads, head_dim, dtype, eps)) != RA_OK) return s;
+  if (n_rows < 1) return fail(RA_EINVAL, "output_impact: n_rows must be >= 1");
+  if ((s = check_tensor("o_stale", o_stale, dtype, n_rows, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("o_fresh", o_fresh, dtype, n_rows, head_dim)) != RA_OK) return s;
+  if (impact == nullptr) return fail(RA_EINVAL, "output_impact: null impact");
+  if ((s = check_workspace("output_impact", workspace, ws_bytes,
+                           refadapt_output_impact_workspace_size(batch, heads, n_rows, head_dim))) != RA_OK)
+    return s;
+  PairSet ps{};
+  ps.cur[0] = view(o_stale);
+  ps.base[0] = view(o_fresh);
+  ps.cur[1] = ps.cur[0];
+  ps.base[1] = ps.base[0];
+  ps.n_rows[0] = ps.n_rows[1] = n_rows;
+  const hipError_t e = launch_pair_change(dtype, batch, heads, head_dim, 1, ps, PAIR_SINGLE, eps, impact, nullptr,
+                                          nullptr, workspace, static_cast<hipStream_t>(stream));
+  return launch_status(e, "output_impact");
+}
+
+ra_status refadapt_mass_mean(int32_t batch, int32_t heads, int32_t n_rows, const float* mass, int32_t complement,
+                             float* out, void* stream) {
+  if (batch < 1 || heads < 1 || n_rows < 1) return fail(RA_EINVAL, "mass_mean: batch, heads, n_rows must be >= 1");
+  if (mass == nullptr || out == nullptr) return fail(RA_EINVAL, "mass_mean: null pointer argument");
+  if (complement != 0 && complement != 1) return fail(RA_EINVAL, "mass_mean: complement must be 0 or 1");
+  const hipError_t e =
+      launch_mass_mean(batch, heads, n_rows, mass, complement, out, static_cast<hipStream_t>(stream));
+  return launch_status(e, "mass_mean");
+}
+
+ra_status refadapt_adjacent_mass_change(int32_t n_steps, int32_t n_blocks, int32_t bh, const float* mass_mean,
+                                        float* out, void* stream) {
+  if (n_steps < 2) return fail(RA_EINVAL, "adjacent_mass_change: n_steps must be >= 2");
+  if (n_blocks < 1 || bh < 1) return fail(RA_EINVAL, "adjacent_mass_change: n_blocks and bh must be >= 1");
+  if (mass_mean == nullptr || out == nullptr) return fail(RA_EINVAL, "adjacent_mass_change: null pointer argument");
+  const hipError_t e =
+      launch_adjacent_change(n_steps, n_blocks, bh, mass_mean, out, static_cast<hipStream_t>(stream));
+  return launch_status(e, "adjacent_mass_change");
+}
+
+}  // extern "C"

@@ -88,6 +88,21 @@ hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, i
                                View v_src, View k_dst, View v_dst, const int32_t* decision, int32_t* age,
                                int32_t step, hipStream_t stream);
 
+// Up to two [B, H, n, d] slice pairs whose relative change the diagnostics
+// reduce in one launch; chunks[] is filled by the launcher.
+struct PairSet {
+  View cur[2], base[2];
+  int32_t n_rows[2];
+  int32_t chunks[2];
+};
+enum { PAIR_SINGLE = 0, PAIR_KV = 1, PAIR_RATIO = 2 };
+size_t pair_workspace_bytes(int32_t B, int32_t H, int32_t head_dim, int npairs, const int32_t* n_rows);
+hipError_t launch_pair_change(int dtype, int32_t B, int32_t H, int32_t head_dim, int npairs, PairSet ps, int kind,
+                              float eps, float* out0, float* out1, float* out2, void* ws, hipStream_t stream);
+hipError_t launch_mass_mean(int32_t B, int32_t H, int32_t n, const float* mass, int complement, float* out,
+                            hipStream_t stream);
+hipError_t launch_adjacent_change(int32_t T, int32_t nb, int32_t bh, const float* m, float* out, hipStream_t stream);
+
 // Launches `kernel` and returns the status of THIS launch (hipLaunchKernel's
 // return value), not a sticky error left by earlier runtime calls. Arguments
 // are converted to the kernel's parameter types before their addresses are

@@ -291,3 +291,122 @@ def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0
         _view("k_cache", k_cache, dt, k_ref.shape), _view("v_cache", v_cache, dt, k_ref.shape),
         _ptr(decision), _ptr(age), int(step), _stream(),
     )
+
+
+# ---- diagnostics sidecar (read-only probes of the controlled path)
+
+
+def _f32_out(name, t, shape, device):
+    if t is None:
+        return torch.empty(shape, dtype=torch.float32, device=device)
+    _on_gpu(name, t)
+    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {tuple(shape)}")
+    return t
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def kv_drift_workspace(k):
+    B, H, n, D = k.shape
+    return torch.empty(max(L.refadapt_kv_drift_workspace_size(B, H, n, D), 8), dtype=torch.uint8, device=k.device)
+
+
+def kv_drift(k_cur, k_base, v_cur, v_base, eps=1e-8, d_k=None, d_v=None, e_kv=None, workspace=None):
+    """Relative change of reference K and V against a base (the anchor for the endpoint
+    drift) and their joint scalar E^KV = (D_K + D_V) / 2, per (b, h), through
+    ``refadapt_kv_drift``. Returns (d_k, d_v, e_kv)."""
+    B, H, n, D = k_cur.shape
+    dt = k_cur.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    d_k = _f32_out("d_k", d_k, (B, H), k_cur.device)
+    d_v = _f32_out("d_v", d_v, (B, H), k_cur.device)
+    e_kv = _f32_out("e_kv", e_kv, (B, H), k_cur.device)
+    workspace = kv_drift_workspace(k_cur) if workspace is None else workspace
+    _on_gpu("workspace", workspace)
+    L.refadapt_kv_drift(
+        B, H, n, D, _DTYPES[dt], _view("k_cur", k_cur, dt), _view("k_base", k_base, dt, k_cur.shape),
+        _view("v_cur", v_cur, dt, k_cur.shape), _view("v_base", v_base, dt, k_cur.shape), float(eps),
+        _ptr(d_k), _ptr(d_v), _ptr(e_kv), _ptr(workspace), _nbytes(workspace), _stream(),
+    )
+    return d_k, d_v, e_kv
+
+
+def drift_log_ratio_workspace(z_ref, z_tgt):
+    B, H, n_ref, D = z_ref.shape
+    nbytes = L.refadapt_drift_log_ratio_workspace_size(B, H, n_ref, z_tgt.shape[2], D)
+    return torch.empty(max(nbytes, 8), dtype=torch.uint8, device=z_ref.device)
+
+
+def drift_log_ratio(z_ref_cur, z_ref_prev, z_tgt_cur, z_tgt_prev, eps=1e-8, d_ref=None, d_tgt=None, rho=None,
+                    workspace=None):
+    """Consecutive drift of the reference and target slices of one of K, V and the matched
+    log-ratio rho = log10((D_ref + eps) / (D_tgt + eps)) per (b, h), through
+    ``refadapt_drift_log_ratio``. Returns (d_ref, d_tgt, rho)."""
+    B, H, n_ref, D = z_ref_cur.shape
+    n_tgt = z_tgt_cur.shape[2]
+    dt = z_ref_cur.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    d_ref = _f32_out("d_ref", d_ref, (B, H), z_ref_cur.device)
+    d_tgt = _f32_out("d_tgt", d_tgt, (B, H), z_ref_cur.device)
+    rho = _f32_out("rho", rho, (B, H), z_ref_cur.device)
+    workspace = drift_log_ratio_workspace(z_ref_cur, z_tgt_cur) if workspace is None else workspace
+    _on_gpu("workspace", workspace)
+    L.refadapt_drift_log_ratio(
+        B, H, n_ref, n_tgt, D, _DTYPES[dt], _view("z_ref_cur", z_ref_cur, dt),
+        _view("z_ref_prev", z_ref_prev, dt, z_ref_cur.shape), _view("z_tgt_cur", z_tgt_cur, dt, (B, H, n_tgt, D)),
+        _view("z_tgt_prev", z_tgt_prev, dt, (B, H, n_tgt, D)), float(eps), _ptr(d_ref), _ptr(d_tgt), _ptr(rho),
+        _ptr(workspace), _nbytes(workspace), _stream(),
+    )
+    return d_ref, d_tgt, rho
+
+
+def output_impact_workspace(o):
+    B, H, n, D = o.shape
+    return torch.empty(max(L.refadapt_output_impact_workspace_size(B, H, n, D), 8), dtype=torch.uint8,
+                       device=o.device)
+
+
+def output_impact(o_stale, o_fresh, eps=1e-8, out=None, workspace=None):
+    """I^KV[b, h] = ||O_stale - O_fresh||_F / (||O_fresh||_F + eps) through ``refadapt_output_impact``."""
+    B, H, n, D = o_stale.shape
+    dt = o_stale.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    out = _f32_out("out", out, (B, H), o_stale.device)
+    workspace = output_impact_workspace(o_stale) if workspace is None else workspace
+    _on_gpu("workspace", workspace)
+    L.refadapt_output_impact(
+        B, H, n, D, _DTYPES[dt], _view("o_stale", o_stale, dt), _view("o_fresh", o_fresh, dt, o_stale.shape),
+        float(eps), _ptr(out), _ptr(workspace), _nbytes(workspace), _stream(),
+    )
+    return out
+
+
+def mass_mean(mass, complement=False, out=None):
+    """Per-(b, h) mean over rows of a [B, H, n] per-query mass (or of 1 - mass) through
+    ``refadapt_mass_mean``."""
+    _on_gpu("mass", mass)
+    if mass.dim() != 3 or mass.dtype != torch.float32 or not mass.is_contiguous():
+        raise ValueError("mass must be a contiguous float32 [B, H, n] tensor")
+    B, H, n = mass.shape
+    out = _f32_out("out", out, (B, H), mass.device)
+    L.refadapt_mass_mean(B, H, n, _ptr(mass), int(bool(complement)), _ptr(out), _stream())
+    return out
+
+
+def adjacent_mass_change(mass_log, out=None):
+    """Per block, 100 / (T - 1) * sum_t |Mbar_t - Mbar_{t-1}| (percentage points) from a
+    [T, n_blocks, ...] log of per-head mass means, through ``refadapt_adjacent_mass_change``."""
+    _on_gpu("mass_log", mass_log)
+    if mass_log.dim() < 2 or mass_log.dtype != torch.float32 or not mass_log.is_contiguous():
+        raise ValueError("mass_log must be a contiguous float32 [T, n_blocks, ...] tensor")
+    T, nb = mass_log.shape[0], mass_log.shape[1]
+    bh = mass_log[0, 0].numel()
+    out = _f32_out("out", out, (nb,), mass_log.device)
+    L.refadapt_adjacent_mass_change(T, nb, bh, _ptr(mass_log), _ptr(out), _stream())
+    return out

@@ -125,3 +125,47 @@ def test_gate_and_commit_validation():
     assert L.LIB.refadapt_cache_commit(1, 2, 10, 100, L.RA_BF16, _t(), _t(), _t(), _t(), None, None, 0, None) == L.RA_EUNSUPPORTED
     # Nothing to copy is not an error.
     assert L.LIB.refadapt_cache_commit(1, 2, 0, 128, L.RA_BF16, _t(), _t(), _t(), _t(), None, None, 0, None) == L.RA_OK
+
+
+def test_diagnostics_validation():
+    p = ctypes.c_void_p(0x1000)
+    ws = L.refadapt_kv_drift_workspace_size(1, 24, 12544, 128)
+    assert ws >= 2 * 24 * 8 and L.refadapt_kv_drift_workspace_size(1, 0, 1, 128) == 0
+    kv = lambda **kw: L.LIB.refadapt_kv_drift(
+        kw.get("B", 1), 24, kw.get("n", 12544), kw.get("d", 128), kw.get("dt", L.RA_BF16), _t(), kw.get("kb", _t()),
+        _t(), _t(), kw.get("eps", 1e-8), None, None, kw.get("e", p), kw.get("ws", ctypes.c_void_p(0x2000)),
+        kw.get("wsb", ws), None)
+    assert kv(wsb=ws - 8) == L.RA_EWORKSPACE
+    assert kv(ws=ctypes.c_void_p(0x2004)) == L.RA_EUNSUPPORTED
+    assert kv(kb=_t(0)) == L.RA_EINVAL and "k_base" in L.refadapt_last_error()
+    assert kv(e=None) == L.RA_EINVAL
+    assert kv(eps=-1.0) == L.RA_EINVAL
+    assert kv(n=0) == L.RA_EINVAL
+    assert kv(d=100) == L.RA_EUNSUPPORTED
+    assert kv(dt=5) == L.RA_EINVAL
+
+    wr = L.refadapt_drift_log_ratio_workspace_size(1, 24, 12544, 4096, 128)
+    assert wr > 0 and L.refadapt_drift_log_ratio_workspace_size(1, 24, 0, 4096, 128) == 0
+    ratio = lambda **kw: L.LIB.refadapt_drift_log_ratio(
+        1, 24, kw.get("nr", 12544), 4096, 128, L.RA_BF16, _t(), _t(), _t(), kw.get("tp", _t()), 1e-8, None, None,
+        kw.get("rho", p), ctypes.c_void_p(0x2000), kw.get("wsb", wr), None)
+    assert ratio(wsb=wr - 8) == L.RA_EWORKSPACE
+    assert ratio(rho=None) == L.RA_EINVAL
+    assert ratio(tp=_t(0x1008)) == L.RA_EUNSUPPORTED
+    assert ratio(nr=0) == L.RA_EINVAL
+
+    wi = L.refadapt_output_impact_workspace_size(1, 24, 4096, 128)
+    assert wi > 0
+    imp = lambda **kw: L.LIB.refadapt_output_impact(
+        1, 24, 4096, 128, L.RA_BF16, _t(), kw.get("of", _t()), 1e-8, kw.get("out", p), ctypes.c_void_p(0x2000),
+        kw.get("wsb", wi), None)
+    assert imp(wsb=0) == L.RA_EWORKSPACE
+    assert imp(out=None) == L.RA_EINVAL
+    assert imp(of=_t(0)) == L.RA_EINVAL
+
+    assert L.LIB.refadapt_mass_mean(1, 24, 0, p, 0, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_mass_mean(1, 24, 10, None, 0, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_mass_mean(1, 24, 10, p, 2, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_adjacent_mass_change(1, 60, 24, p, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_adjacent_mass_change(8, 0, 24, p, p, None) == L.RA_EINVAL
+    assert L.LIB.refadapt_adjacent_mass_change(8, 60, 24, None, p, None) == L.RA_EINVAL
