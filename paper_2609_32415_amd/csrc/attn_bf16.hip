@@ -13,9 +13,9 @@
 // row-major V tile with ds_read_b64_tr_b16 (LDS transpose read).
 //
 // Software pipeline (per wavefront): iteration j issues the 16 MFMAs of S_{j+1}
-// each followed by a slice of the softmax of S_j (phase A), then the 16 MFMAs
-// of O += V_j^T P_j^T, under the first half of which the probabilities of the
-// second half of P_j are formed (phase B). sched_barrier fences keep that
+// each followed by one pair of probabilities of S_j (phase A: pairs 0..9), then
+// the 16 MFMAs of O += V_j^T P_j^T, under the first six of which the remaining
+// pairs 10..15 are formed (phase B). sched_barrier fences keep that
 // order, so the vector ALU works while the matrix core runs. K tiles run one
 // tile ahead of V tiles through two LDS buffers each, refilled from registers:
 // the next K tile is loaded at the top of the iteration, the next V tile at the
@@ -27,11 +27,17 @@
 // staged in LDS (two 16-byte chunks per thread per tile). Staging V only over
 // phase B keeps the register peak of phase A under that limit.
 //
-// Online softmax in the exp2 domain with lazy rescaling: a lane moves its
-// running max only when a tile's max exceeds it by more than 2^8, so the O
-// rescale is almost never executed; probabilities are then bounded by 2^8.
-// Row sums add the fp32 probabilities (two chains per lane), so the reference
-// mass and the log-sum-exp carry no bf16 rounding.
+// Online softmax in the exp2 domain without a per-tile row max: probabilities
+// are formed against the running max m, and a lane's partial row sum bounds
+// each of its terms, so a sum within 2^12 proves that every probability is at
+// most 2^12 and m may stay. The test runs (wave-wide, NaN and inf failing it)
+// once for pairs 0..9 before any of them enters O and once for pairs 8..15
+// (P blocks 2 and 3) before the first MFMA that reads them; when it fails (always at a
+// workgroup's first tile, where m = -inf), a cold path takes the row max of
+// the scores still to be formed, rescales O and l, and forms them again. The
+// O rescale and the row max are thus almost never executed.
+// Row sums add the fp32 probabilities, so the reference mass and the
+// log-sum-exp carry no bf16 rounding.
 //
 // Split statistics for the reference mass (paper Sec. 3.2, directional
 // exposure): after the last reference tile the running (max, sum) pair is
@@ -69,7 +75,7 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 constexpr int BM = kAttnBf16BM;  // query rows per workgroup
 constexpr int BN = kAttnBf16BN;  // keys per LDS tile
 constexpr int NT = 512;          // threads per workgroup
-constexpr float TAU = 8.0f;      // lazy-rescale threshold (log2 units)
+constexpr float PBOUND = 4096.0f;  // bound on a probability against the running max (2^12)
 
 // Row permutation of a 32-key MFMA block: swaps bits 2 and 3 of the row index.
 // With key sigma(m) in A-row m of S^T = K Q^T, output register r of lane-half g
@@ -314,21 +320,32 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       return *reinterpret_cast<const bf16x8*>(kb + k_lane + 32 * (i / KS) * KROW + 16 * (i % KS));
     };
     uint32_t pw[4][4];  // packed bf16 probabilities: P block s2, keys 16*s2 + 8*g + 2w, +1
-    float rs0 = 0.f, rs1 = 0.f, mx0 = 0.f, m_new = m_run;
+    // Row-sum chains: pairs 0..7 (P blocks 0, 1) and pairs 8..15 (P blocks 2, 3).
+    float rs_a = 0.f, rs_b = 0.f, m_new = m_run;
     auto prob_pair = [&](int q) {  // scores 2q, 2q+1 -> P block q/4, word q%4
       const int mb = q >> 3, o2 = (2 * q) & 15;
       const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m_new));
       const float e1 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2 + 1], c, -m_new));
-      rs0 += e0;
-      rs1 += e1;
+      float& rs = q < 8 ? rs_a : rs_b;
+      rs += e0 + e1;
       bf16x2 pr;
       pr[0] = (__bf16)e0;
       pr[1] = (__bf16)e1;
       uint32_t w = __builtin_bit_cast(uint32_t, pr);
       pin(w);
-      pin(rs0);
-      pin(rs1);
+      pin(rs);
       pw[q >> 2][q & 3] = w;
+    };
+    // Row max of the lane's scores in key blocks mb0..1, shared by the lane pair of a query.
+    auto tile_max = [&](int mb0) {
+      float m = s_cur[1][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) m = fmaxf(m, s_cur[1][r]);
+      if (mb0 == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) m = fmaxf(m, s_cur[0][r]);
+      }
+      return xor32_max(m) * c;
     };
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb) s_next[mb] = f32x16{};
@@ -336,37 +353,32 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) ka[i] = k_operand(i);
     __builtin_amdgcn_sched_barrier(0);
+    // Probabilities against the running max: a lane's partial row sum bounds each of its
+    // terms, so a sum within PBOUND (NaN and inf fail the test) proves that none exceeds
+    // it and the running max may stay; otherwise a cold path moves the max.
 #pragma unroll
     for (int i = 0; i < NQK; ++i) {
       s_next[i / KS] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i & 3], qreg[i % KS], s_next[i / KS], 0, 0, 0);
       if (i + 4 < NQK) ka[i & 3] = k_operand(i + 4);
-      if (i == 0) {
-        float m = s_cur[0][0];
-#pragma unroll
-        for (int r = 1; r < 16; ++r) m = fmaxf(m, s_cur[0][r]);
-        mx0 = m;
-      } else if (i == 1) {
-        float m = mx0;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, s_cur[1][r]);
-        m = xor32_max(m) * c;
-        m_new = m > m_run + TAU ? m : m_run;  // lazy: move only on a large increase
-        pin(m_new);
-      } else if (i - 2 < 8) {
-        prob_pair(i - 2);  // pairs 0..7 fill P blocks 0 and 1
-      }
+      if (i < 10) prob_pair(i);  // P blocks 0, 1 and half of block 2
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (NQK < 10) {  // head_dim 64: fewer MFMAs than softmax slices
+    if (NQK < 10) {  // head_dim 64: fewer MFMAs than slices
 #pragma unroll
-      for (int q = NQK - 2; q < 8; ++q) prob_pair(q);
+      for (int q = NQK; q < 10; ++q) prob_pair(q);
     }
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 1 unless the max moved
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
+    if (__any(!(rs_a + rs_b <= PBOUND))) {
+      // Rare (always at a workgroup's first tile): move the max to the tile's row max
+      // (nothing of this tile is in O^T yet) and form pairs 0..9 again.
+      m_new = fmaxf(tile_max(0), m_run);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
       for (int i = 0; i < DB; ++i) o[i] *= alpha;
+      m_run = m_new;
+      rs_a = rs_b = 0.f;
+#pragma unroll
+      for (int q = 0; q < 10; ++q) prob_pair(q);
     }
 
     // ---- phase B: O^T += V_j^T P_j^T, P block-major; the probabilities of P blocks
@@ -391,15 +403,31 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       o[i % DB] =
           __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], __builtin_bit_cast(bf16x8, pwv), o[i % DB], 0, 0, 0);
       if (i + 2 < NPV) va[(i + 2) % 3] = v_operand(i + 2);
-      // pairs 8..15 fill P blocks 2 and 3 before the first MFMA that reads them
-      if (DB == 4 && i < 8) prob_pair(8 + i);
-      if (DB == 2 && i < 4) {
-        prob_pair(8 + 2 * i);
-        prob_pair(9 + 2 * i);
+      // pairs 10..15 complete P blocks 2 and 3 before the first MFMA that reads them
+      if (DB == 4 && i < 6) prob_pair(10 + i);
+      if (DB == 2 && i < 3) {
+        prob_pair(10 + 2 * i);
+        prob_pair(11 + 2 * i);
       }
       __builtin_amdgcn_sched_barrier(0);
+      if (i == 2 * DB - 1 && __any(!(rs_b <= PBOUND))) {
+        // Rare: pairs 8..15 exceed the bound. O^T holds this tile's P blocks 0 and 1
+        // against the old max: rescale it with l and their sum, then form P blocks 2
+        // and 3 against the new max before their MFMAs. Blocks 0 and 1 passed the first
+        // test and only shrink, so the max of key block 1 suffices.
+        m_new = fmaxf(tile_max(1), m_run);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
+        rs_a *= alpha;
+#pragma unroll
+        for (int k = 0; k < DB; ++k) o[k] *= alpha;
+        m_run = m_new;
+        rs_b = 0.f;
+#pragma unroll
+        for (int q = 8; q < 16; ++q) prob_pair(q);
+      }
     }
-    l_run += xor32_add(rs0 + rs1);
+    l_run += xor32_add(rs_a + rs_b);
 
     if (j == n_rt - 1) {  // end of the reference segment: freeze its statistics
       m_ref = m_run;
@@ -475,10 +503,14 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 }
 
 // Combines the key chunks of split query tiles: one row per D/4 threads, four
-// output columns per thread. With M the largest running max over the chunks,
-//   L_R = sum_c l_R,c 2^(m_R,c - M),  L_Y = sum_c l_Y,c 2^(m_c - M),
-//   o = sum_c O_c 2^(m_c - M) / (L_R + L_Y),  mass = L_R / (L_R + L_Y).
-// A chunk's reference max never exceeds its running max, so M bounds both.
+// output columns per thread. With M the largest running max over the chunks and
+// M_R the largest reference max,
+//   L'_R = sum_c l_R,c 2^(m_R,c - M_R),  L_R = L'_R 2^(M_R - M),
+//   L_Y = sum_c l_Y,c 2^(m_c - M),  o = sum_c O_c 2^(m_c - M) / (L_R + L_Y),
+//   mass = L_R / (L_R + L_Y),  lse_ref = M_R + log2 L'_R (times ln 2).
+// A chunk's reference max never exceeds its running max, so M bounds both;
+// summing the reference part against M_R keeps lse_ref finite when the target
+// keys score so far above the reference keys that 2^(M_R - M) underflows.
 template <int D>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   constexpr int TPR = D / 4, RPB = 256 / TPR;
@@ -500,22 +532,27 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   if (qrow >= n_rows) return;
 
   const int64_t base = (int64_t)st * pl.chunks * BM + rr;  // partial row of chunk 0
-  float M = -__builtin_inff();
-  for (int c = 0; c < pl.chunks; ++c) M = fmaxf(M, p.part_st[base + (int64_t)c * BM].x);
-  float L_R = 0.f, L_Y = 0.f;
+  float M = -__builtin_inff(), M_R = -__builtin_inff();
+  for (int c = 0; c < pl.chunks; ++c) {
+    const float4 sv = p.part_st[base + (int64_t)c * BM];
+    M = fmaxf(M, sv.x);
+    if (sv.w > 0.f) M_R = fmaxf(M_R, sv.z);
+  }
+  float L_Rr = 0.f, L_Y = 0.f;  // L_Rr: reference sum against M_R
   float4 acc{0.f, 0.f, 0.f, 0.f};
   for (int c = 0; c < pl.chunks; ++c) {
     const int64_t prow = base + (int64_t)c * BM;
     const float4 sv = p.part_st[prow];
     const float wgt = __builtin_amdgcn_exp2f(sv.x - M);
     L_Y += sv.y * wgt;
-    if (sv.w > 0.f) L_R += sv.w * __builtin_amdgcn_exp2f(sv.z - M);
+    if (sv.w > 0.f) L_Rr += sv.w * __builtin_amdgcn_exp2f(sv.z - M_R);
     const float4 ov = *reinterpret_cast<const float4*>(p.part_o + prow * D + col);
     acc.x += ov.x * wgt;
     acc.y += ov.y * wgt;
     acc.z += ov.z * wgt;
     acc.w += ov.w * wgt;
   }
+  const float L_R = L_Rr > 0.f ? L_Rr * __builtin_amdgcn_exp2f(M_R - M) : 0.f;
   const float total = L_R + L_Y;
   const float inv = 1.f / total;
   const View& ov = ref_rows ? p.o_ref : p.o_tgt;
@@ -537,7 +574,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
       if (p.mass_tgt) p.mass_tgt[row] = mass;
       if (p.lse_tgt) {
         const float ln2 = 0.69314718055994531f;
-        p.lse_tgt[2 * row] = (M + __log2f(L_R)) * ln2;
+        p.lse_tgt[2 * row] = (M_R + __log2f(L_Rr)) * ln2;
         p.lse_tgt[2 * row + 1] = (M + __log2f(total)) * ln2;
       }
     } else if (p.mass_refq) {

@@ -276,3 +276,60 @@ def test_full_size_sampled_rows(name, qset, kvsrc):
         rr = synth.sample_rows(w.n_ref, 48, 4)
         refr = joint_attention(x["q_ref"][:, :, rr], kr, vr, x["k_tgt"], x["v_tgt"])
         assert max_abs(host(got.o_ref[:, :, rr]), refr["o"]) <= O_TOL["bf16"]
+
+
+def _jump_inputs(d, pattern, n_ref=600, n_tgt=300, H=2, seed=11):
+    """Inputs whose row max rises sharply at chosen keys: every query gets a component c along
+    a unit direction u and chosen keys get B u, so their logits stand far above the rest.
+    ``spikes``: keys at offset 10 of reference tile 3 (first key block of a tile), offset 48 of
+    reference tile 5 (second key block) and offset 56 of target tile 1 (after the reference
+    statistics are frozen), each higher than the last; ``ramp``: every key gets a component
+    growing with its index, so the max rises at every tile; ``huge``: one spike far beyond
+    the fp32 range of 2^(logit - running max)."""
+    _, x = _inputs("bf16", d, n_ref, n_tgt, 1, H, seed=seed, bias=False)
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    x = {k: v.astype(np.float64) for k, v in x.items()}
+    for k in ("q_tgt", "q_ref"):
+        x[k] = x[k] + 2.0 * u
+    n = n_ref + n_tgt
+    k_all = np.concatenate([x["k_ref"], x["k_tgt"]], axis=2)
+    if pattern == "spikes":
+        for idx, b in ((3 * 64 + 10, 100.0), (5 * 64 + 48, 200.0), (n_ref + 64 + 56, 400.0)):
+            k_all[:, :, idx, :] += b * u
+    elif pattern == "ramp":
+        k_all += (np.arange(n) / n * 400.0)[None, None, :, None] * u
+    else:  # huge: about 2^700 above the running max in the exp2 domain
+        k_all[:, :, 7 * 64 + 50, :] += 2000.0 * u
+    x["k_ref"], x["k_tgt"] = k_all[:, :, :n_ref], k_all[:, :, n_ref:]
+    x["k_ref_cache"] = x["k_ref"]
+    x["v_ref_cache"] = x["v_ref"]
+    return {k: synth.round_to_dtype(v, "bf16") for k, v in x.items()}
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("pattern", ["spikes", "ramp", "huge"])
+@pytest.mark.parametrize("mode", [("target", "fresh"), ("all", "fresh")], ids=lambda m: "/".join(m))
+@pytest.mark.parametrize("split", [True, False], ids=["split", "whole"])
+def test_running_max_moves(d, pattern, mode, split):
+    """The probabilities are formed against the running max and the max moves only when a
+    lane's partial row sum leaves its bound; these inputs force every such path (first and
+    second half of a tile, after the reference freeze, at every tile, with overflow)."""
+    qset, kvsrc = mode
+    print(f"running max d{d} {pattern} {qset}/{kvsrc} split={split}", flush=True)
+    x = _jump_inputs(d, pattern)
+    got = _gpu(x, "bf16", qset, kvsrc, **({} if split else {"workspace": False}))
+    ref = _oracle(x, qset, False)
+    assert np.all(np.isfinite(host(got.o_tgt)))
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    lse = host(got.lse)
+    # The lse bar scales with the logit magnitude here: the fp32 accumulation of q.k in the
+    # MFMA carries a relative error, and these logits reach hundreds.
+    tol = 1e-3 * max(1.0, float(np.abs(ref["tgt"]["lse_all"]).max()) / 100)
+    assert max_abs(lse[..., 0], ref["tgt"]["lse_ref"]) <= tol
+    assert max_abs(lse[..., 1], ref["tgt"]["lse_all"]) <= tol
+    if qset == "all":
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
+        assert max_abs(host(got.ref_mass_refq), ref["ref"]["ref_mass"]) <= MASS_TOL["bf16"]
