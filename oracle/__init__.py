@@ -16,6 +16,8 @@ joint_attention      Sec. 3.3 fresh/stale-output equations + Sec. 3.2
 joint_attention_loops
                      The same definition as explicit Python loops, for tiny
                      shapes (brute force).
+segment_masses       Per-query mass on each reference segment (the exposure of
+                     one reference image).
 q_change             Sec. 3.1 consecutive-drift equation applied to post-RoPE
                      target queries per head (Sec. 4, runtime cues).
 head_exposure        Sec. 3.2 directional-exposure equation: mean over target
@@ -40,7 +42,7 @@ hand-derived fixtures under ``tests/golden/`` and structural statements of
 the paper.
 """
 
-from .joint_attention import joint_attention, joint_attention_loops
+from .joint_attention import joint_attention, joint_attention_loops, segment_masses
 from .stats import q_change, head_exposure, gate, GateResult, REUSE, REACTIVATE, COMPUTE
 from .controller import run_controller, local_impact, ControllerTrace
 from . import diagnostics
@@ -48,6 +50,7 @@ from . import diagnostics
 __all__ = [
     "joint_attention",
     "joint_attention_loops",
+    "segment_masses",
     "q_change",
     "head_exposure",
     "gate",

@@ -113,3 +113,25 @@ def joint_attention_loops(q, k_ref, v_ref, k_tgt, v_tgt, scale=None):
                 if n_ref > 0:
                     lse_ref[b, h, i] = math.log(ref_total)
     return {"o": o, "ref_mass": ref_mass, "lse_ref": lse_ref, "lse_all": lse_all}
+
+
+def segment_masses(q, k_ref, k_tgt, seg_end, scale=None):
+    """Per-query softmax mass on each reference segment (Sec. 3.2 directional exposure,
+    restricted to the keys of one segment).
+
+    ``seg_end`` lists the exclusive end row of each segment inside the reference rows
+    (the last one is n_ref). Returns ``[..., n_q, n_seg]`` fp64: the sum of the softmax
+    row over the keys of each segment, from the same logits as ``joint_attention``.
+    """
+    q, k_ref, k_tgt = map(_as64, (q, k_ref, k_tgt))
+    d = q.shape[-1]
+    s = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    ends = list(seg_end)
+    if not ends or ends[-1] != k_ref.shape[-2] or any(b <= a for a, b in zip([0] + ends[:-1], ends)):
+        raise ValueError("segment ends must increase to n_ref")
+    k = np.concatenate([k_ref, k_tgt], axis=-2)
+    logits = s * np.matmul(q, np.swapaxes(k, -1, -2))
+    p = np.exp(logits - logits.max(axis=-1, keepdims=True))
+    a = p / p.sum(axis=-1, keepdims=True)
+    starts = [0] + ends[:-1]
+    return np.stack([a[..., lo:hi].sum(axis=-1) for lo, hi in zip(starts, ends)], axis=-1)

@@ -182,3 +182,38 @@ def test_large_logits_do_not_overflow():
     # weights e^5000 : e^4900 : e^-1000 -> mass = 1 / (1 + e^-100 + ...)
     assert np.isfinite(out["o"]).all()
     np.testing.assert_allclose(out["ref_mass"], 1.0 / (1.0 + math.exp(-100.0)), rtol=1e-15)
+
+
+def test_segment_masses_closed_forms():
+    """Collinear keys: segment s (n_s keys at a_s e1), target (n_y keys at b e1), query c e1 ->
+    mass_s = n_s e^{x_s} / (sum_s n_s e^{x_s} + n_y e^{y}) with x_s = scale c a_s, y = scale c b."""
+    from oracle import segment_masses
+
+    d, sizes, mags, n_y, b, c = 16, (3, 5, 2), (1.0, -2.0, 4.0), 7, 0.5, 1.5
+    e1 = np.zeros(d)
+    e1[0] = 1.0
+    kr = np.concatenate([np.tile(m * e1, (n, 1)) for n, m in zip(sizes, mags)])[None, None]
+    kt = np.tile(b * e1, (n_y, 1))[None, None]
+    q = np.tile(c * e1, (4, 1))[None, None]
+    s = 1.0 / np.sqrt(d)
+    w = np.array([n * np.exp(s * c * m) for n, m in zip(sizes, mags)])
+    want = w / (w.sum() + n_y * np.exp(s * c * b))
+    got = segment_masses(q, kr, kt, np.cumsum(sizes).tolist())
+    np.testing.assert_allclose(got[0, 0], np.tile(want, (4, 1)), rtol=1e-13)
+
+
+def test_segment_masses_uniform_sum_and_permutation():
+    from oracle import joint_attention, segment_masses
+
+    rng = np.random.default_rng(12)
+    q = rng.standard_normal((1, 2, 5, 8))
+    np.testing.assert_allclose(segment_masses(q, np.zeros((1, 2, 10, 8)), np.zeros((1, 2, 6, 8)), [4, 10]),
+                               np.broadcast_to([4 / 16, 6 / 16], (1, 2, 5, 2)), rtol=1e-14)
+    kr, kt = rng.standard_normal((1, 2, 9, 8)), rng.standard_normal((1, 2, 4, 8))
+    m = segment_masses(q, kr, kt, [3, 9])
+    ref = joint_attention(q, kr, np.zeros_like(kr), kt, np.zeros_like(kt))["ref_mass"]
+    np.testing.assert_allclose(m.sum(axis=-1), ref, rtol=1e-13)
+    swapped = segment_masses(q, np.concatenate([kr[..., 3:, :], kr[..., :3, :]], axis=-2), kt, [6, 9])
+    np.testing.assert_allclose(swapped[..., ::-1], m, rtol=1e-13)
+    with pytest.raises(ValueError):
+        segment_masses(q, kr, kt, [3, 8])
