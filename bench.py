@@ -60,6 +60,8 @@ def parse_args():
     ap.add_argument("--sweep", action="store_true", help="also run the 60-block x 8-step controller sweep")
     ap.add_argument("--diagnostics", action="store_true",
                     help="also run the diagnostics sidecar over a 60-block x 8-step controller trajectory")
+    ap.add_argument("--segments", action="store_true",
+                    help="also run the per-reference exposure / individual stale impact table")
     ap.add_argument("--ref-sweep", action="store_true",
                     help="also run the reference-count sweep (1..8 reference images at single-reference shapes)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -328,6 +330,10 @@ def main():
         from paper_2609_32415_amd.controller import run_diagnostics
 
         out["diagnostics"] = run_diagnostics(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+    if args.segments:
+        from paper_2609_32415_amd.controller import run_reference_segments
+
+        out["reference_segments"] = run_reference_segments(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
     if args.ref_sweep:
         from paper_2609_32415_amd.controller import run_ref_count_sweep
 

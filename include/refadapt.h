@@ -52,11 +52,17 @@ typedef enum {
 typedef enum {
   RA_KV_FRESH = 0, /* k_ref / v_ref (this step's reference K/V) */
   RA_KV_CACHE = 1, /* k_cache / v_cache (the block cache of Sec. 4) */
-  RA_KV_DEVICE = 2 /* chosen on the device from *decision (ra_decision):
-                    *   REUSE      -> target queries only, cached K/V
-                    *   REACTIVATE -> all queries, cached K/V
-                    *   COMPUTE    -> all queries, fresh K/V */
+  RA_KV_DEVICE = 2, /* chosen on the device from *decision (ra_decision):
+                     *   REUSE      -> target queries only, cached K/V
+                     *   REACTIVATE -> all queries, cached K/V
+                     *   COMPUTE    -> all queries, fresh K/V */
+  RA_KV_SEGMENTS = 3 /* per reference segment (ra_attn_args.seg_*): segment s
+                      * reads the cached K/V when bit s of seg_cache is set,
+                      * else the fresh K/V (bf16 only) */
 } ra_kvsrc;
+
+/* Most reference segments (e.g. reference images and text) one call can tell apart. */
+#define RA_MAX_SEG 16
 
 /* Block decisions of Alg. 1 (monotone depth-adaptive reference reuse). */
 typedef enum { RA_REUSE = 0, RA_REACTIVATE = 1, RA_COMPUTE = 2 } ra_decision;
@@ -101,6 +107,12 @@ typedef struct {
   float* ref_mass_refq;          /* out [B, H, n_ref] reference-query mass on reference keys, or NULL */
   void* workspace;               /* device scratch for key-split partial results, or NULL (no split) */
   size_t workspace_bytes;        /* its size; >= refadapt_joint_attn_workspace_size(desc) when non-NULL */
+  /* Reference segments (used with RA_KV_SEGMENTS or a non-NULL seg_mass; else ignored):
+   * segment s holds reference rows [seg_end[s-1], seg_end[s]) (seg_end[-1] = 0). */
+  int32_t n_seg;                 /* 1..RA_MAX_SEG */
+  int32_t seg_end[RA_MAX_SEG];   /* increasing; multiples of 64 except seg_end[n_seg-1] == n_ref */
+  uint32_t seg_cache;            /* RA_KV_SEGMENTS: bit s selects the cached K/V for segment s */
+  float* seg_mass;               /* out [B, H, n_tgt, n_seg] target-query mass per segment, or NULL */
 } ra_attn_args;
 
 /*
@@ -124,6 +136,18 @@ typedef struct {
  * read *decision first: on RA_REUSE only target query rows are computed and
  * o_ref is left untouched.
  *
+ * Reference segments (bf16): the reference rows may be split into n_seg
+ * segments (the reference images and the text; App. "probe non-intrusiveness
+ * and multi-reference controls": the references are not interchangeable).
+ * Under RA_KV_SEGMENTS each segment reads fresh or cached K/V as seg_cache
+ * says, so one launch evaluates a stale cache for any subset of the
+ * references. seg_mass[b, h, q, s] = sum over the keys k of segment s of A_qk
+ * (the directional exposure of Sec. 3.2 restricted to one segment); the
+ * segments' masses add up to ref_mass. Segment boundaries must fall on 64-row
+ * key tiles (the last one is n_ref), and under RA_KV_SEGMENTS the fresh and
+ * cached K (and V) views must share their strides. With seg_mass the launch
+ * never splits key ranges (the workspace is not used).
+ *
  * Load balance (bf16): with a workspace, query tiles of a last, partly filled
  * round of workgroups are split into key-tile ranges whose partial softmax
  * statistics a second kernel merges (the same rescale-and-add the online
@@ -138,8 +162,11 @@ typedef struct {
  * or a required pointer that is NULL (q/k/v/o_tgt always; k_ref/v_ref when
  * fresh K/V may be read and n_ref > 0; k_cache/v_cache when cached K/V may be
  * read and n_ref > 0; q_ref/o_ref when reference queries may attend and
- * n_ref > 0; decision under RA_KV_DEVICE). RA_EUNSUPPORTED for head_dim not
- * in {64, 128} or misaligned tensors or workspace. RA_EWORKSPACE for a
+ * n_ref > 0; decision under RA_KV_DEVICE; n_seg outside 1..RA_MAX_SEG or
+ * segment ends that do not increase to n_ref). RA_EUNSUPPORTED for head_dim not
+ * in {64, 128} or misaligned tensors or workspace, and for segments with
+ * RA_F32, RA_KV_DEVICE, an inner boundary off the 64-row key tiles, or (under
+ * RA_KV_SEGMENTS) fresh and cached views with different strides. RA_EWORKSPACE for a
  * non-NULL workspace smaller than refadapt_joint_attn_workspace_size(desc).
  */
 ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream);

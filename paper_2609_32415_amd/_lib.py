@@ -26,7 +26,8 @@ RA_BF16, RA_F32 = 0, 1
 # ra_qset
 RA_Q_TARGET, RA_Q_ALL = 0, 1
 # ra_kvsrc
-RA_KV_FRESH, RA_KV_CACHE, RA_KV_DEVICE = 0, 1, 2
+RA_KV_FRESH, RA_KV_CACHE, RA_KV_DEVICE, RA_KV_SEGMENTS = 0, 1, 2, 3
+RA_MAX_SEG = 16
 # ra_decision
 RA_REUSE, RA_REACTIVATE, RA_COMPUTE = 0, 1, 2
 # ra_gate_mode
@@ -95,6 +96,10 @@ class ra_attn_args(ctypes.Structure):
         ("ref_mass_refq", ctypes.c_void_p),
         ("workspace", ctypes.c_void_p),
         ("workspace_bytes", ctypes.c_size_t),
+        ("n_seg", ctypes.c_int32),
+        ("seg_end", ctypes.c_int32 * RA_MAX_SEG),
+        ("seg_cache", ctypes.c_uint32),
+        ("seg_mass", ctypes.c_void_p),
     ]
 
 

@@ -554,3 +554,94 @@ def run_ref_count_sweep(device="cuda:0", counts=(1, 2, 3, 4, 5, 6, 7, 8), n_bloc
                         f"N_Y 4096; product gate at theta_q {theta_q} x theta_m {theta_m}",
             "rows": rows}
 
+
+
+def run_reference_segments(device="cuda:0", weights=(1.0, 0.5, 0.0, 1.0), sizes=(4096, 4096, 4096, 256),
+                           cache_noise=0.02, log=None):
+    """Per-reference exposure and individual stale impact at the multi-reference shapes.
+
+    The reference rows are three 4096-token images and 256 text tokens. The synthetic key
+    bias is weighted per segment (``weights``), so the references draw different attention,
+    and the cache is the fresh reference K/V plus one drift step of ``cache_noise``. For
+    each reference s: its exposure (per-head mean over target queries of the mass on its
+    keys, from one fresh launch with per-segment masses) and its individual stale impact
+    I^KV_s (target output with only segment s read from the cache against the fresh output,
+    through ``RA_KV_SEGMENTS``); then the all-stale impact, the same table with the first
+    two images swapped (the references are not interchangeable: values follow the image,
+    not its position), and the time of a segment launch against a plain cached launch.
+    """
+    import numpy as np
+
+    w = synth.workload("multi_ref", n_ref=sum(sizes), ref_segments=tuple(sizes), ref_bias_weights=tuple(weights),
+                       cache_noise=cache_noise)
+    x = synth.block_inputs(w)
+    cache = synth.stale_cache(w, x)
+    ends = np.cumsum(sizes).tolist()
+    n_seg = len(sizes)
+
+    def table(order):
+        perm = np.concatenate([np.arange(e - n, e) for n, e in ((sizes[i], ends[i]) for i in order)])
+        bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device).to(torch.bfloat16)
+        t = {k: bf(v) for k, v in x.items() if k.endswith("_tgt")}
+        kr, vr = bf(x["k_ref"][:, :, perm]), bf(x["v_ref"][:, :, perm])
+        kc, vc = bf(cache["k_ref"][:, :, perm]), bf(cache["v_ref"][:, :, perm])
+        ends_p = np.cumsum([sizes[i] for i in order]).tolist()
+        fresh = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, seg_end=ends_p, seg_mass=True,
+                               workspace=False)
+        expo = [ops.mass_mean(fresh.seg_mass[..., s].contiguous()) for s in range(n_seg)]
+        imp = []
+        for s in range(n_seg):
+            o_s = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, k_cache=kc, v_cache=vc,
+                                 kvsrc="segments", seg_end=ends_p, seg_cache=[i == s for i in range(n_seg)]).o_tgt
+            imp.append(ops.output_impact(o_s, fresh.o_tgt))
+        o_all = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=kc, v_cache=vc, kvsrc="cache",
+                               workspace=False).o_tgt
+        imp_all = ops.output_impact(o_all, fresh.o_tgt)
+        torch.cuda.synchronize()
+        # rows in the original image order
+        back = np.argsort(order)
+        ex = np.array([float(e.mean()) for e in expo])[back]
+        im = np.array([float(i.mean()) for i in imp])[back]
+        return ex, im, float(imp_all.mean()), (t, kr, vr, kc, vc, ends_p)
+
+    ex, im, im_all, (t, kr, vr, kc, vc, ends_p) = table(list(range(n_seg)))
+    order2 = [1, 0] + list(range(2, n_seg))
+    ex2, im2, im_all2, _ = table(order2)
+
+    def timed(fn, n=20):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    mixed = [i % 2 == 0 for i in range(n_seg)]
+    ws = ops.attn_workspace(t["q_tgt"], sum(sizes), "target", "cache")
+    ms_cache = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=kc, v_cache=vc,
+                                            kvsrc="cache", workspace=ws))
+    ms_cache_whole = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=kc, v_cache=vc,
+                                                  kvsrc="cache", workspace=False))
+    ms_seg = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, k_cache=kc,
+                                          v_cache=vc, kvsrc="segments", seg_end=ends_p, seg_cache=mixed))
+    ms_seg_mass = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, k_cache=kc,
+                                               v_cache=vc, kvsrc="segments", seg_end=ends_p, seg_cache=mixed,
+                                               seg_mass=True))
+    names = [f"image{i}" for i in range(n_seg - 1)] + ["text"]
+    res = {
+        "segments": names, "sizes": list(sizes), "bias_weights": list(weights), "cache_noise": cache_noise,
+        "exposure": [round(v, 5) for v in ex], "individual_stale_impact": [round(v, 6) for v in im],
+        "all_stale_impact": round(im_all, 6), "exposure_sum": round(float(ex.sum()), 5),
+        "swapped_first_two": {"exposure": [round(v, 5) for v in ex2],
+                              "individual_stale_impact": [round(v, 6) for v in im2],
+                              "all_stale_impact": round(im_all2, 6)},
+        "reuse_attention_ms": {"cache_split": round(ms_cache, 4), "cache_whole": round(ms_cache_whole, 4),
+                               "segments_mixed": round(ms_seg, 4), "segments_mixed_with_seg_mass": round(ms_seg_mass, 4)},
+    }
+    if log:
+        log(f"reference segments: exposure {res['exposure']}, individual stale impact "
+            f"{res['individual_stale_impact']}, all-stale {res['all_stale_impact']}")
+    return res

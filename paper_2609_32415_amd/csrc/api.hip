@@ -150,7 +150,7 @@ ra_status check_attn_desc(const ra_attn_desc* desc, const char* who) {
   if (d.n_ref < 0) return fail(RA_EINVAL, "%s: n_ref must be >= 0 (got %d)", who, d.n_ref);
   if (d.dtype != RA_BF16 && d.dtype != RA_F32) return fail(RA_EINVAL, "%s: unknown dtype %d", who, d.dtype);
   if (d.qset != RA_Q_TARGET && d.qset != RA_Q_ALL) return fail(RA_EINVAL, "%s: unknown qset %d", who, d.qset);
-  if (d.kvsrc < RA_KV_FRESH || d.kvsrc > RA_KV_DEVICE) return fail(RA_EINVAL, "%s: unknown kvsrc %d", who, d.kvsrc);
+  if (d.kvsrc < RA_KV_FRESH || d.kvsrc > RA_KV_SEGMENTS) return fail(RA_EINVAL, "%s: unknown kvsrc %d", who, d.kvsrc);
   if (d.head_dim != 64 && d.head_dim != 128)
     return fail(RA_EUNSUPPORTED, "%s: head_dim %d not supported (64 or 128)", who, d.head_dim);
   if (!std::isfinite(d.scale)) return fail(RA_EINVAL, "%s: scale must be finite", who);
@@ -183,8 +183,30 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   const ra_attn_args& a = *args;
   const bool device = d.kvsrc == RA_KV_DEVICE;
   const bool ref_queries = (device || d.qset == RA_Q_ALL) && d.n_ref > 0;
-  const bool reads_fresh = d.n_ref > 0 && (d.kvsrc == RA_KV_FRESH || device);
-  const bool reads_cache = d.n_ref > 0 && (d.kvsrc == RA_KV_CACHE || device);
+  // Reference segments: per-segment K/V sources or per-segment masses.
+  const bool seg = d.kvsrc == RA_KV_SEGMENTS || a.seg_mass != nullptr;
+  uint32_t seg_cache = 0;
+  if (seg) {
+    if (d.dtype != RA_BF16) return fail(RA_EUNSUPPORTED, "joint_attn: reference segments need RA_BF16");
+    if (device) return fail(RA_EUNSUPPORTED, "joint_attn: reference segments are not available under RA_KV_DEVICE");
+    if (d.n_ref < 1) return fail(RA_EINVAL, "joint_attn: reference segments need n_ref >= 1");
+    if (a.n_seg < 1 || a.n_seg > RA_MAX_SEG)
+      return fail(RA_EINVAL, "joint_attn: n_seg %d outside 1..%d", a.n_seg, RA_MAX_SEG);
+    int32_t prev = 0;
+    for (int i = 0; i < a.n_seg; ++i) {
+      const int32_t e = a.seg_end[i];
+      if (e <= prev) return fail(RA_EINVAL, "joint_attn: seg_end[%d] = %d does not increase", i, e);
+      if (i + 1 < a.n_seg && e % kAttnBf16BN != 0)
+        return fail(RA_EUNSUPPORTED, "joint_attn: seg_end[%d] = %d is not a multiple of %d", i, e, kAttnBf16BN);
+      prev = e;
+    }
+    if (prev != d.n_ref) return fail(RA_EINVAL, "joint_attn: seg_end[n_seg-1] = %d != n_ref %d", prev, d.n_ref);
+    const uint32_t all = (1u << a.n_seg) - 1u;
+    seg_cache = d.kvsrc == RA_KV_SEGMENTS ? (a.seg_cache & all) : d.kvsrc == RA_KV_CACHE ? all : 0u;
+  }
+  const bool reads_fresh =
+      d.n_ref > 0 && (d.kvsrc == RA_KV_FRESH || device || (d.kvsrc == RA_KV_SEGMENTS && seg_cache != ((1u << a.n_seg) - 1u)));
+  const bool reads_cache = d.n_ref > 0 && (d.kvsrc == RA_KV_CACHE || device || (d.kvsrc == RA_KV_SEGMENTS && seg_cache != 0));
   if ((s = check_tensor("q_tgt", a.q_tgt, d.dtype, d.n_tgt, d.head_dim)) != RA_OK) return s;
   if ((s = check_tensor("k_tgt", a.k_tgt, d.dtype, d.n_tgt, d.head_dim)) != RA_OK) return s;
   if ((s = check_tensor("v_tgt", a.v_tgt, d.dtype, d.n_tgt, d.head_dim)) != RA_OK) return s;
@@ -202,6 +224,13 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
     if ((s = check_tensor("o_ref", a.o_ref, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
   }
   if (device && a.decision == nullptr) return fail(RA_EINVAL, "joint_attn: RA_KV_DEVICE needs a decision pointer");
+  if (d.kvsrc == RA_KV_SEGMENTS && reads_fresh && reads_cache) {
+    const auto same = [](const ra_tensor& x, const ra_tensor& y) {
+      return x.stride_b == y.stride_b && x.stride_h == y.stride_h && x.stride_s == y.stride_s;
+    };
+    if (!same(a.k_ref, a.k_cache) || !same(a.v_ref, a.v_cache))
+      return fail(RA_EUNSUPPORTED, "joint_attn: RA_KV_SEGMENTS needs the fresh and cached K/V to share strides");
+  }
 
   AttnParams p{};
   p.q_tgt = view(a.q_tgt);
@@ -228,7 +257,8 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   const float scale = d.scale > 0.f ? d.scale : 1.0f / std::sqrt((float)d.head_dim);
   p.sc_log2 = scale * 1.4426950408889634f;
 
-  const LaunchPlan lp = plan_launch(d, a.workspace != nullptr);
+  // Per-segment statistics need whole query tiles; per-segment sources alone may split.
+  const LaunchPlan lp = plan_launch(d, a.workspace != nullptr && a.seg_mass == nullptr);
   const int64_t total = (int64_t)d.batch * d.heads * (lp.qt_ref + lp.qt_tgt);
   if (total > 0x7fffffff) return fail(RA_EUNSUPPORTED, "joint_attn: problem too large for one launch");
   if (a.workspace != nullptr) {
@@ -244,6 +274,23 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   p.plan[1] = lp.plan[1];
   p.part_o = static_cast<float*>(a.workspace);
   p.part_st = lp.ws_bytes ? reinterpret_cast<float4*>(static_cast<char*>(a.workspace) + lp.part_o_bytes) : nullptr;
+  if (seg) {
+    p.n_seg = a.n_seg;
+    for (int i = 0; i < a.n_seg; ++i) {
+      p.seg_tile_end[i] = (a.seg_end[i] + kAttnBf16BN - 1) / kAttnBf16BN;
+      const bool c = (seg_cache >> i) & 1u;
+      p.seg_kbase[i] = c ? a.k_cache.data : a.k_ref.data;
+      p.seg_vbase[i] = c ? a.v_cache.data : a.v_ref.data;
+    }
+    p.seg_cache = seg_cache;
+    p.seg_mass = a.seg_mass;
+    // The kernel applies one set of strides to both sources: those of the fresh views when
+    // any segment reads them, else those of the cached views.
+    if (!reads_fresh) {
+      p.k_fresh = p.k_cache;
+      p.v_fresh = p.v_cache;
+    }
+  }
 
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const hipError_t e = d.dtype == RA_BF16 ? launch_attn_bf16(p, d.head_dim, st) : launch_attn_f32(p, d.head_dim, st);

@@ -156,7 +156,9 @@ __device__ __forceinline__ void stage_store(const Staging<D>& st, uint16_t* tile
   for (int i = 0; i < Layout<D>::NCH; ++i) *reinterpret_cast<u32x4*>(tile + lds_off + i * STEP) = st.r[i];
 }
 
-template <int D>
+// SEG: reference segments: each reference key tile reads the fresh or the cached K/V of its
+// segment; with seg_mass (whole tiles only) each segment's log-sum-exp is recorded.
+template <int D, bool SEG>
 __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // MFMA k-steps over the head dim for S^T
   constexpr int DB = D / 32;   // 32-row blocks of the O^T accumulator
@@ -203,11 +205,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const bool ref_rows = qt < qt_ref;
   if (!ref_rows) qt -= qt_ref;
 
-  const View& qv = ref_rows ? p.q_ref : p.q_tgt;
-  const View& ov = ref_rows ? p.o_ref : p.o_tgt;
+  const View qv = ref_rows ? p.q_ref : p.q_tgt;
+  const View ov = ref_rows ? p.o_ref : p.o_tgt;
   const int n_rows = ref_rows ? p.n_ref : p.n_tgt;
-  const View& krv = use_cache ? p.k_cache : p.k_fresh;
-  const View& vrv = use_cache ? p.v_cache : p.v_fresh;
+  const View krv = use_cache ? p.k_cache : p.k_fresh;
+  const View vrv = use_cache ? p.v_cache : p.v_fresh;
   const uint16_t* kr = static_cast<const uint16_t*>(krv.p) + b * krv.sb + h * krv.sh;
   const uint16_t* vr = static_cast<const uint16_t*>(vrv.p) + b * vrv.sb + h * vrv.sh;
   const uint16_t* ky = static_cast<const uint16_t*>(p.k_tgt.p) + b * p.k_tgt.sb + h * p.k_tgt.sh;
@@ -224,8 +226,38 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int ROWS_PER_STEP = NT / KCH;
   const int k_st = ((st_row & ~31) | sigma(st_row & 31)) * KROW + st_ch * 8;
   const int v_st = st_row * VROW + st_ch * 8;
+  // SEG: each of the K and V streams visits reference tiles in increasing order, so it keeps
+  // its current segment and that segment's end tile, and reads a segment end from the
+  // kernel arguments only when it crosses one.
+  // The cursor keeps the segment's base pointer (this (b, h) applied) and end tile and
+  // reads the next ones from the kernel arguments only when it crosses a segment end.
+  int kseg = 0, kend = 0, vseg = 0, vend = 0;
+  const uint16_t *kbase = nullptr, *vbase = nullptr;
+  const int64_t kbh = b * krv.sb + h * krv.sh, vbh = b * vrv.sb + h * vrv.sh;
+  if constexpr (SEG) {
+    kend = vend = p.seg_tile_end[0];
+    kbase = static_cast<const uint16_t*>(p.seg_kbase[0]) + kbh;
+    vbase = static_cast<const uint16_t*>(p.seg_vbase[0]) + vbh;
+  }
+  // Stages reference tile j of one of K, V (strides ss, lane offset voff) from the base of
+  // its segment.
+  auto load_ref_seg = [&](Staging<D>& st, int j, int& seg, int& end, const uint16_t*& base,
+                          const void* const* seg_base, int64_t bh_off, int64_t ss, uint32_t voff) {
+    while (j >= end && seg + 1 < p.n_seg) {
+      end = p.seg_tile_end[++seg];
+      base = static_cast<const uint16_t*>(seg_base[seg]) + bh_off;
+    }
+    stage_load<D>(st, tile_rsrc<D>(base + (int64_t)j * BN * ss, ss, tile_valid(j)), voff,
+                  (uint32_t)(ROWS_PER_STEP * ss * 2));
+  };
   auto load_k = [&](Staging<D>& st, int j) {
     const int valid = tile_valid(j);
+    if constexpr (SEG) {
+      if (j < n_rt) {
+        load_ref_seg(st, j, kseg, kend, kbase, p.seg_kbase, kbh, krv.ss, voff_r);
+        return;
+      }
+    }
     if (j < n_rt) {
       stage_load<D>(st, tile_rsrc<D>(kr + (int64_t)j * BN * krv.ss, krv.ss, valid), voff_r,
                     (uint32_t)(ROWS_PER_STEP * krv.ss * 2));
@@ -236,6 +268,12 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   };
   auto load_v = [&](Staging<D>& st, int j) {
     const int valid = tile_valid(j);
+    if constexpr (SEG) {
+      if (j < n_rt) {
+        load_ref_seg(st, j, vseg, vend, vbase, p.seg_vbase, vbh, vrv.ss, voff_rv);
+        return;
+      }
+    }
     if (j < n_rt) {
       stage_load<D>(st, tile_rsrc<D>(vr + (int64_t)j * BN * vrv.ss, vrv.ss, valid), voff_rv,
                     (uint32_t)(ROWS_PER_STEP * vrv.ss * 2));
@@ -293,6 +331,9 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   float m_run = -__builtin_inff(), l_run = 0.f;
   float m_ref = -__builtin_inff(), l_ref = 0.f;
   const float c = p.sc_log2;
+  // SEG: current reference segment, the key tile that ends it, and this row's seg_mass offset.
+  int seg_idx = 0, seg_end_t = SEG && n_rt > 0 ? p.seg_tile_end[0] : -1;
+  const int64_t seg_row = ((int64_t)bh * p.n_tgt + qrow) * p.n_seg;
 
   auto iteration = [&](int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
     const int jb = (j - j0) & 1;  // LDS buffer of K_j and V_j
@@ -326,14 +367,18 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       const int mb = q >> 3, o2 = (2 * q) & 15;
       const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m_new));
       const float e1 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2 + 1], c, -m_new));
-      float& rs = q < 8 ? rs_a : rs_b;
-      rs += e0 + e1;
+      if (q < 8) {
+        rs_a += e0 + e1;
+        pin(rs_a);
+      } else {
+        rs_b += e0 + e1;
+        pin(rs_b);
+      }
       bf16x2 pr;
       pr[0] = (__bf16)e0;
       pr[1] = (__bf16)e1;
       uint32_t w = __builtin_bit_cast(uint32_t, pr);
       pin(w);
-      pin(rs);
       pw[q >> 2][q & 3] = w;
     };
     // Row max of the lane's scores in key blocks mb0..1, shared by the lane pair of a query.
@@ -429,7 +474,18 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     }
     l_run += xor32_add(rs_a + rs_b);
 
-    if (j == n_rt - 1) {  // end of the reference segment: freeze its statistics
+    if (SEG && p.seg_mass) {  // per-segment statistics (whole tiles only)
+      if (j + 1 == seg_end_t) {  // end of reference segment seg_idx
+        // Record its log-sum-exp (log2 domain; the epilogue turns it into a mass), then
+        // fold its sum into the reference statistics, each kept against its own max.
+        if (!ref_rows && qvalid && g == 0) p.seg_mass[seg_row + seg_idx] = m_run + __log2f(l_run);
+        l_ref = seg_idx == 0 ? l_run : l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) + l_run;
+        m_ref = m_run;
+        l_run = 0.f;
+        ++seg_idx;
+        seg_end_t = seg_idx < p.n_seg ? p.seg_tile_end[seg_idx] : -1;
+      }
+    } else if (j == n_rt - 1) {  // end of the reference segment: freeze its statistics
       m_ref = m_run;
       l_ref = l_run;
       l_run = 0.f;
@@ -498,6 +554,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       } else if (p.mass_refq) {
         p.mass_refq[row] = mass;
       }
+      if (SEG && p.seg_mass && !ref_rows) {  // per-segment log-sum-exp -> mass, in place
+        const float lt = m_run + __log2f(total);
+        for (int s2 = 0; s2 < p.n_seg; ++s2)
+          p.seg_mass[seg_row + s2] = __builtin_amdgcn_exp2f(p.seg_mass[seg_row + s2] - lt);
+      }
     }
   }
 }
@@ -555,7 +616,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const float L_R = L_Rr > 0.f ? L_Rr * __builtin_amdgcn_exp2f(M_R - M) : 0.f;
   const float total = L_R + L_Y;
   const float inv = 1.f / total;
-  const View& ov = ref_rows ? p.o_ref : p.o_tgt;
+  const View ov = ref_rows ? p.o_ref : p.o_tgt;
   const int b = bh / p.H, h = bh - b * p.H;
   uint16_t* op = static_cast<uint16_t*>(const_cast<void*>(ov.p)) + b * ov.sb + h * ov.sh + (int64_t)qrow * ov.ss;
   union {
@@ -597,8 +658,8 @@ AttnSlots attn_bf16_slots(int head_dim) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return AttnSlots{0, 0};
   const hipError_t e =
       head_dim == 128
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<128>, NT, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<64>, NT, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<128, false>, NT, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<64, false>, NT, 0);
   if (e != hipSuccess || per_cu < 1 || cus < 1) return AttnSlots{0, 0};
   if (dev < 64) {
     cache[dev][di][1].store(per_cu, std::memory_order_relaxed);
@@ -611,8 +672,13 @@ hipError_t launch_attn_bf16(const AttnParams& p, int head_dim, hipStream_t strea
   const int items = max(p.plan[0].total_items, p.plan[1].total_items);
   if (items <= 0) return hipSuccess;
   const dim3 grid(items), block(NT);
-  hipError_t e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128>, grid, block, 0, stream, p)
-                                 : launch_kernel(attn_bf16_kernel<64>, grid, block, 0, stream, p);
+  hipError_t e;
+  if (p.n_seg > 0)
+    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, true>, grid, block, 0, stream, p)
+                        : launch_kernel(attn_bf16_kernel<64, true>, grid, block, 0, stream, p);
+  else
+    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, false>, grid, block, 0, stream, p)
+                        : launch_kernel(attn_bf16_kernel<64, false>, grid, block, 0, stream, p);
   if (e != hipSuccess) return e;
   const int split = max(p.plan[0].split_tiles, p.plan[1].split_tiles);
   if (split == 0) return hipSuccess;

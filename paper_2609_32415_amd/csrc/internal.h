@@ -15,7 +15,8 @@ struct View {
   int64_t sb, sh, ss;
 };
 
-enum { KV_FRESH = 0, KV_CACHE = 1, KV_DEVICE = 2 };
+enum { KV_FRESH = 0, KV_CACHE = 1, KV_DEVICE = 2, KV_SEGMENTS = 3 };
+constexpr int kMaxSeg = 16;
 enum { DEC_REUSE = 0, DEC_REACTIVATE = 1, DEC_COMPUTE = 2 };
 
 // Work decomposition of one bf16 attention launch over its query tiles (all
@@ -49,6 +50,17 @@ struct AttnParams {
   SplitPlan plan[2];
   float* part_o;     // [items][BM][head_dim] unnormalised fp32 partial outputs of split items
   float4* part_st;   // [items][BM] (m, l_tgt, m_ref, l_ref) per partial row
+  // Reference segments (bf16; seg_mass needs whole tiles): n_seg > 0 selects the segment
+  // kernel. Segment s covers reference key tiles [seg_tile_end[s-1], seg_tile_end[s]);
+  // seg_cache bit s reads the cached K/V for it; seg_mass [B, H, n_tgt, n_seg] or null.
+  int32_t n_seg;
+  int32_t seg_tile_end[kMaxSeg];
+  uint32_t seg_cache;
+  float* seg_mass;
+  // Per segment, the base of the K and V view it reads (fresh or cached; both views share
+  // their strides, which are those of k_fresh / v_fresh).
+  const void* seg_kbase[kMaxSeg];
+  const void* seg_vbase[kMaxSeg];
 };
 
 // Query rows per workgroup of each attention kernel (the host sizes the grid with

@@ -18,7 +18,7 @@ from . import _lib as L
 
 _DTYPES = {torch.bfloat16: L.RA_BF16, torch.float32: L.RA_F32}
 _QSET = {"target": L.RA_Q_TARGET, "all": L.RA_Q_ALL}
-_KVSRC = {"fresh": L.RA_KV_FRESH, "cache": L.RA_KV_CACHE, "device": L.RA_KV_DEVICE}
+_KVSRC = {"fresh": L.RA_KV_FRESH, "cache": L.RA_KV_CACHE, "device": L.RA_KV_DEVICE, "segments": L.RA_KV_SEGMENTS}
 _GATE = {"product": L.RA_GATE_PRODUCT, "q_only": L.RA_GATE_Q_ONLY, "mass_only": L.RA_GATE_MASS_ONLY, "and": L.RA_GATE_AND}
 
 REUSE, REACTIVATE, COMPUTE = L.RA_REUSE, L.RA_REACTIVATE, L.RA_COMPUTE
@@ -63,6 +63,7 @@ class AttnOut:
     ref_mass: Optional[torch.Tensor]
     lse: Optional[torch.Tensor]
     ref_mass_refq: Optional[torch.Tensor]
+    seg_mass: Optional[torch.Tensor] = None
 
 
 def joint_attn(
@@ -86,6 +87,9 @@ def joint_attn(
     lse=False,
     ref_mass_refq=False,
     workspace=None,
+    seg_end=None,
+    seg_cache=None,
+    seg_mass=False,
 ):
     """Joint attention over [K_R; K_Y] through ``refadapt_joint_attn``.
 
@@ -94,6 +98,12 @@ def joint_attn(
     workspace the library asks for (torch caching allocator), False runs
     without key splits, a uint8 device tensor is used as given (see
     ``attn_workspace``). Returns an ``AttnOut``.
+
+    Reference segments (bf16): ``seg_end`` lists each segment's end row in R
+    (multiples of 64 except the last, which is n_ref). With ``kvsrc="segments"``
+    ``seg_cache`` (one bool per segment) picks the cached K/V for a segment, else
+    the fresh K/V. ``seg_mass`` (bool or preallocated fp32 ``[B, H, n_tgt, n_seg]``)
+    returns each target query's mass per segment in ``AttnOut.seg_mass``.
     """
     B, H, n_tgt, D = q_tgt.shape
     dt = q_tgt.dtype
@@ -122,6 +132,15 @@ def joint_attn(
     mass_t = _opt(ref_mass, (B, H, n_tgt))
     lse_t = _opt(lse, (B, H, n_tgt, 2))
     mrq_t = _opt(ref_mass_refq, (B, H, n_ref)) if n_ref > 0 else None
+    n_seg = 0 if seg_end is None else len(seg_end)
+    if (kvsrc == "segments" or seg_mass is not False) and not 1 <= n_seg <= L.RA_MAX_SEG:
+        raise ValueError(f"seg_end must list 1..{L.RA_MAX_SEG} segment ends")
+    smass_t = _opt(seg_mass, (B, H, n_tgt, n_seg)) if n_seg else None
+    cache_bits = 0
+    if kvsrc == "segments":
+        if seg_cache is None or len(seg_cache) != n_seg:
+            raise ValueError("seg_cache must give one flag per segment")
+        cache_bits = sum(1 << i for i, c in enumerate(seg_cache) if c)
     if decision is not None:
         _on_gpu("decision", decision)
         if decision.dtype != torch.int32:
@@ -155,9 +174,13 @@ def joint_attn(
         ref_mass_refq=None if mrq_t is None else mrq_t.data_ptr(),
         workspace=ws_ptr,
         workspace_bytes=ws_bytes,
+        n_seg=n_seg,
+        seg_end=(ctypes.c_int32 * L.RA_MAX_SEG)(*(list(seg_end or []) + [0] * (L.RA_MAX_SEG - n_seg))),
+        seg_cache=cache_bits,
+        seg_mass=None if smass_t is None else smass_t.data_ptr(),
     )
     L.refadapt_joint_attn(desc, args, _stream())
-    return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t)
+    return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t, smass_t)
 
 
 def attn_workspace(q_tgt, n_ref, qset="target", kvsrc="fresh"):

@@ -60,6 +60,10 @@ class Workload:
     cache_noise: float = 0.0  # std of the perturbation that makes a stale cache differ from fresh
     theta_q: tuple = ()
     theta_m: tuple = ()
+    # Optional reference segments (row counts, e.g. reference images then text) and a weight
+    # per segment on the key bias, so that the segments draw different attention.
+    ref_segments: tuple = ()
+    ref_bias_weights: tuple = ()
     meta: dict = field(default_factory=dict, compare=False, hash=False)
 
     @property
@@ -155,6 +159,11 @@ def _apply_key_bias(w, block, t):
     target_comp = np.where(shared, 1.0, -lam[None, :, None])  # [B, H, n_tgt]
     uq = u[:, :, None, :].astype(np.float32)
     k_bias = (0.5 * math.sqrt(d) * u[:, :, None, :]).astype(np.float32)
+    if w.ref_bias_weights:  # per-segment weights on the bias (rows of R in segment order)
+        if len(w.ref_bias_weights) != len(w.ref_segments) or sum(w.ref_segments) != w.n_ref:
+            raise ValueError("ref_bias_weights needs one weight per segment of ref_segments summing to n_ref")
+        wt = np.repeat(np.asarray(w.ref_bias_weights, dtype=np.float32), w.ref_segments)
+        k_bias = k_bias * wt[None, None, :, None]
     t["k_ref"] += k_bias
     q = t["q_tgt"]
     cur = np.einsum("bhnd,bhd->bhn", q, u.astype(np.float32))

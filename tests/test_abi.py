@@ -169,3 +169,30 @@ def test_diagnostics_validation():
     assert L.LIB.refadapt_adjacent_mass_change(1, 60, 24, p, p, None) == L.RA_EINVAL
     assert L.LIB.refadapt_adjacent_mass_change(8, 0, 24, p, p, None) == L.RA_EINVAL
     assert L.LIB.refadapt_adjacent_mass_change(8, 60, 24, None, p, None) == L.RA_EINVAL
+
+
+def test_segment_validation():
+    """Reference-segment arguments are checked before anything is launched."""
+    def args(n_seg, ends, mass=True, cache=0):
+        a = L.ra_attn_args(q_tgt=_t(), k_tgt=_t(), v_tgt=_t(), q_ref=_t(), k_ref=_t(), v_ref=_t(), k_cache=_t(),
+                           v_cache=_t(), o_tgt=_t(), o_ref=_t())
+        a.n_seg = n_seg
+        for i, e in enumerate(ends):
+            a.seg_end[i] = e
+        a.seg_cache = cache
+        a.seg_mass = 0x3000 if mass else None
+        return a
+    seg = lambda **kw: _desc(**{"n_ref": 300, "kvsrc": L.RA_KV_SEGMENTS, **kw})
+    call = lambda d, a: L.LIB.refadapt_joint_attn(ctypes.byref(d), ctypes.byref(a), None)
+    assert call(seg(dtype=L.RA_F32, head_dim=64), args(2, [128, 300])) == L.RA_EUNSUPPORTED
+    assert call(_desc(n_ref=300, kvsrc=L.RA_KV_DEVICE), args(2, [128, 300])) == L.RA_EUNSUPPORTED
+    assert call(seg(), args(2, [100, 300])) == L.RA_EUNSUPPORTED and "multiple of 64" in L.refadapt_last_error()
+    assert call(seg(), args(2, [128, 299])) == L.RA_EINVAL
+    assert call(seg(), args(2, [128, 128])) == L.RA_EINVAL
+    assert call(seg(), args(0, [])) == L.RA_EINVAL
+    assert call(seg(), args(17, [64 * (i + 1) for i in range(16)])) == L.RA_EINVAL
+    assert call(seg(n_ref=0), args(1, [0])) == L.RA_EINVAL
+    # Fresh and cached views with different strides cannot share one segment launch.
+    a2 = args(2, [128, 300], mass=False, cache=1)
+    a2.k_cache = _t(ss=256)
+    assert call(seg(), a2) == L.RA_EUNSUPPORTED and "strides" in L.refadapt_last_error()

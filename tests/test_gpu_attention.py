@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from gpu_helpers import MASS_TOL, O_TOL, dev, host, max_abs
-from oracle import joint_attention
+from oracle import joint_attention, segment_masses
 from paper_2609_32415_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -176,7 +176,7 @@ def _workspace_bytes(n_ref, n_tgt, H, d, qset, kvsrc):
     from paper_2609_32415_amd import _lib as L
 
     desc = L.ra_attn_desc(1, H, d, n_ref, n_tgt, L.RA_BF16, 0.0, {"target": 0, "all": 1}[qset],
-                          {"fresh": 0, "cache": 1, "device": 2}[kvsrc])
+                          {"fresh": 0, "cache": 1, "device": 2, "segments": 3}[kvsrc])
     return L.refadapt_joint_attn_workspace_size(desc)
 
 
@@ -333,3 +333,87 @@ def test_running_max_moves(d, pattern, mode, split):
     if qset == "all":
         assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
         assert max_abs(host(got.ref_mass_refq), ref["ref"]["ref_mass"]) <= MASS_TOL["bf16"]
+
+
+# Reference segments: d, segment sizes (rows of R), n_tgt, H, cached segments.
+SEG_CASES = [
+    (128, (128, 192, 37), 200, 2, (True, False, True)),
+    (64, (64, 64, 64, 100), 150, 3, (False, True, False, True)),
+    (128, (300,), 100, 2, (True,)),
+    (128, (64,) * 8 + (40,), 128, 2, (True, False) * 4 + (True,)),
+    (128, (256, 256), 333, 2, (False, False)),
+]
+
+
+def _seg_oracle_inputs(x, sizes, cached):
+    """Reference K/V assembled per segment from the cached or the fresh rows."""
+    ends = np.cumsum(sizes)
+    kr, vr = x["k_ref"].copy(), x["v_ref"].copy()
+    for lo, hi, c in zip(np.concatenate([[0], ends[:-1]]), ends, cached):
+        if c:
+            kr[..., lo:hi, :] = x["k_ref_cache"][..., lo:hi, :]
+            vr[..., lo:hi, :] = x["v_ref_cache"][..., lo:hi, :]
+    return kr, vr, ends.tolist()
+
+
+@pytest.mark.parametrize("case", SEG_CASES, ids=lambda c: f"d{c[0]}-{len(c[1])}seg")
+@pytest.mark.parametrize("qset", ["target", "all"])
+def test_reference_segments_parity(case, qset):
+    """RA_KV_SEGMENTS: each segment reads its own K/V source; per-segment masses match the
+    oracle and add up to the reference mass."""
+    d, sizes, n_tgt, H, cached = case
+    print(f"segments d{d} sizes {sizes} cached {cached} {qset}", flush=True)
+    _, x = _inputs("bf16", d, sum(sizes), n_tgt, 1, H)
+    kr, vr, ends = _seg_oracle_inputs(x, sizes, cached)
+    got = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached, seg_mass=True)
+    ref = joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"])
+    sm = segment_masses(x["q_tgt"], kr, x["k_tgt"], ends)
+    assert max_abs(host(got.o_tgt), ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["ref_mass"]) <= MASS_TOL["bf16"]
+    lse = host(got.lse)
+    assert max_abs(lse[..., 0], ref["lse_ref"]) <= 1e-3
+    assert max_abs(lse[..., 1], ref["lse_all"]) <= 1e-3
+    assert max_abs(host(got.seg_mass), sm) <= MASS_TOL["bf16"]
+    assert max_abs(host(got.seg_mass).sum(-1), host(got.ref_mass)) <= 1e-5
+    if qset == "all":
+        rr = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
+        assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]
+        assert max_abs(host(got.ref_mass_refq), rr["ref_mass"]) <= MASS_TOL["bf16"]
+
+
+@pytest.mark.parametrize("kvsrc", ["fresh", "cache"])
+def test_segment_mass_with_one_source(kvsrc):
+    """seg_mass under RA_KV_FRESH / RA_KV_CACHE: all segments read that source; the output,
+    mass and lse equal those of the same launch without segments."""
+    sizes = (64, 128, 90)
+    _, x = _inputs("bf16", 128, sum(sizes), 300, 1, 2)
+    ends = np.cumsum(sizes).tolist()
+    got = _gpu(x, "bf16", "target", kvsrc, seg_end=ends, seg_mass=True)
+    plain = _gpu(x, "bf16", "target", kvsrc, workspace=False)
+    use = kvsrc == "cache"
+    kr = x["k_ref_cache"] if use else x["k_ref"]
+    np.testing.assert_allclose(host(got.seg_mass), segment_masses(x["q_tgt"], kr, x["k_tgt"], ends),
+                               atol=MASS_TOL["bf16"], rtol=0)
+    assert max_abs(host(got.o_tgt), host(plain.o_tgt)) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), host(plain.ref_mass)) <= 1e-5
+
+
+@pytest.mark.parametrize("qset", ["target", "all"])
+def test_reference_segments_key_split(qset):
+    """Per-segment sources without seg_mass may split key ranges: chunks that start inside a
+    segment pick up its source; results match the oracle and the unsplit launch."""
+    sizes, cached = (256, 384, 360), (True, False, True)
+    assert _workspace_bytes(sum(sizes), 100, 2, 128, qset, "segments") > 0, "the launch should split key ranges"
+    _, x = _inputs("bf16", 128, sum(sizes), 100, 1, 2)
+    kr, vr, ends = _seg_oracle_inputs(x, sizes, cached)
+    got = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached)
+    whole = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached, workspace=False)
+    ref = joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"])
+    assert max_abs(host(got.o_tgt), ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["ref_mass"]) <= MASS_TOL["bf16"]
+    lse = host(got.lse)
+    assert max_abs(lse[..., 0], ref["lse_ref"]) <= 1e-3 and max_abs(lse[..., 1], ref["lse_all"]) <= 1e-3
+    assert max_abs(host(got.o_tgt), host(whole.o_tgt)) <= O_TOL["bf16"]
+    if qset == "all":
+        rr = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
+        assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]

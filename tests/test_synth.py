@@ -3,6 +3,7 @@
 import hashlib
 
 import numpy as np
+import pytest
 import torch
 
 from paper_2609_32415_amd import synth
@@ -61,3 +62,18 @@ def test_key_bias_sets_target_component():
         assert ok.all()
         frac = np.isclose(vals, 1.0, atol=1e-4).mean()
         assert 0.15 < frac < 0.45 or lam == 1.0
+
+
+def test_per_segment_key_bias_weights():
+    """Weights scale the reference-key bias per segment; no weights leaves the inputs unchanged."""
+    base = synth.workload("tiny", dtype="bf16", heads=2, head_dim=64, n_ref=192, n_tgt=64, key_bias=True)
+    w = synth.workload("tiny", dtype="bf16", heads=2, head_dim=64, n_ref=192, n_tgt=64, key_bias=True,
+                       ref_segments=(128, 64), ref_bias_weights=(1.0, 0.0))
+    a, b = synth.base_tensors(base), synth.base_tensors(w)
+    np.testing.assert_array_equal(a["k_ref"][:, :, :128], b["k_ref"][:, :, :128])
+    unbiased = synth.workload("tiny", dtype="bf16", heads=2, head_dim=64, n_ref=192, n_tgt=64, key_bias=False)
+    np.testing.assert_array_equal(b["k_ref"][:, :, 128:], synth.base_tensors(unbiased)["k_ref"][:, :, 128:])
+    np.testing.assert_array_equal(a["q_tgt"], b["q_tgt"])
+    with pytest.raises(ValueError):
+        synth.base_tensors(synth.workload("tiny", n_ref=192, key_bias=True, ref_segments=(100,),
+                                          ref_bias_weights=(1.0,)))
