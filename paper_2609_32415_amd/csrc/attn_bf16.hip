@@ -214,6 +214,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const uint16_t* vr = static_cast<const uint16_t*>(vrv.p) + b * vrv.sb + h * vrv.sh;
   const uint16_t* ky = static_cast<const uint16_t*>(p.k_tgt.p) + b * p.k_tgt.sb + h * p.k_tgt.sh;
   const uint16_t* vy = static_cast<const uint16_t*>(p.v_tgt.p) + b * p.v_tgt.sb + h * p.v_tgt.sh;
+  int64_t kr_ss = krv.ss, vr_ss = vrv.ss, ky_ss = p.k_tgt.ss, vy_ss = p.v_tgt.ss;
 
   auto tile_valid = [&](int j) { return j < n_rt ? min(BN, p.n_ref - j * BN) : min(BN, p.n_tgt - (j - n_rt) * BN); };
   // Per-thread staging offsets (bytes into a tile, per segment) and LDS offsets.
@@ -259,11 +260,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       }
     }
     if (j < n_rt) {
-      stage_load<D>(st, tile_rsrc<D>(kr + (int64_t)j * BN * krv.ss, krv.ss, valid), voff_r,
-                    (uint32_t)(ROWS_PER_STEP * krv.ss * 2));
+      stage_load<D>(st, tile_rsrc<D>(kr + (int64_t)j * BN * kr_ss, kr_ss, valid), voff_r,
+                    (uint32_t)(ROWS_PER_STEP * kr_ss * 2));
     } else {
-      stage_load<D>(st, tile_rsrc<D>(ky + (int64_t)(j - n_rt) * BN * p.k_tgt.ss, p.k_tgt.ss, valid), voff_yk,
-                    (uint32_t)(ROWS_PER_STEP * p.k_tgt.ss * 2));
+      stage_load<D>(st, tile_rsrc<D>(ky + (int64_t)(j - n_rt) * BN * ky_ss, ky_ss, valid), voff_yk,
+                    (uint32_t)(ROWS_PER_STEP * ky_ss * 2));
     }
   };
   auto load_v = [&](Staging<D>& st, int j) {
@@ -275,11 +276,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       }
     }
     if (j < n_rt) {
-      stage_load<D>(st, tile_rsrc<D>(vr + (int64_t)j * BN * vrv.ss, vrv.ss, valid), voff_rv,
-                    (uint32_t)(ROWS_PER_STEP * vrv.ss * 2));
+      stage_load<D>(st, tile_rsrc<D>(vr + (int64_t)j * BN * vr_ss, vr_ss, valid), voff_rv,
+                    (uint32_t)(ROWS_PER_STEP * vr_ss * 2));
     } else {
-      stage_load<D>(st, tile_rsrc<D>(vy + (int64_t)(j - n_rt) * BN * p.v_tgt.ss, p.v_tgt.ss, valid), voff_yv,
-                    (uint32_t)(ROWS_PER_STEP * p.v_tgt.ss * 2));
+      stage_load<D>(st, tile_rsrc<D>(vy + (int64_t)(j - n_rt) * BN * vy_ss, vy_ss, valid), voff_yv,
+                    (uint32_t)(ROWS_PER_STEP * vy_ss * 2));
     }
   };
 
@@ -337,6 +338,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 
   auto iteration = [&](int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
     const int jb = (j - j0) & 1;  // LDS buffer of K_j and V_j
+    // Keep the per-workgroup tile sources in registers: rematerialising them from the kernel
+    // arguments would put a scalar load under the first MFMA's LDS wait.
+    asm volatile("" : "+s"(kr), "+s"(vr), "+s"(ky), "+s"(vy));
+    asm volatile("" : "+s"(kr_ss), "+s"(vr_ss), "+s"(ky_ss), "+s"(vy_ss));
     // Global loads for the tiles this iteration stages: K_{j+2} here, V_{j+1} at the
     // start of phase B. Past the workgroup's last key tile the index is clamped to
     // it: the reload lands in a buffer that is never read again.
