@@ -358,6 +358,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         }
     }
 
+    // Issue priority: the first wavefront on a SIMD (waves 0-3) otherwise wins every tie,
+    // finishes its tile early and waits at the barrier while its partner runs alone. The
+    // partner gets the higher priority in phase A and the first one in phase B.
+    const bool partner = __builtin_amdgcn_readfirstlane(wave) >= 4;
+    if (partner) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
     // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by a slice
     // of the softmax of S_j: the row max, then the probabilities of P blocks 0 and 1.
     // At the last iteration the K buffer holds no tile and S_{j+1} is discarded.
@@ -434,6 +439,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // ---- phase B: O^T += V_j^T P_j^T, P block-major; the probabilities of P blocks
     // 2 and 3 are formed under the MFMAs of blocks 0 and 1. V^T operands come from
     // LDS transpose reads issued two MFMAs ahead.
+    if (partner) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
     load_v(stv, min(j + 1, j1 - 1));
     const uint16_t* vs = vbuf[jb];
     auto v_operand = [&](int i) {  // i = DB * s2 + db
