@@ -130,7 +130,9 @@ typedef struct {
  * log-sum-exp of the scaled logits over reference keys / all keys (lse_ref is
  * -inf when n_ref == 0). Outputs are written in `dtype` (accumulation is fp32,
  * bf16 MFMA for RA_BF16). Writing ref_mass / lse does not change o (the
- * attention output is bit-identical with them on or off).
+ * attention output is bit-identical with them on or off). Requesting seg_mass
+ * folds the reference sums segment by segment, so o then differs from the
+ * launch without it by fp32 rounding only.
  *
  * Under RA_KV_DEVICE the launch is sized for every query and the workgroups
  * read *decision first: on RA_REUSE only target query rows are computed and
