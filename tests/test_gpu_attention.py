@@ -417,3 +417,61 @@ def test_reference_segments_key_split(qset):
     if qset == "all":
         rr = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
         assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]
+
+
+def _random_cases(n=24, seed=2024):
+    """Seeded random configurations: head dim, ragged reference/target sizes (including
+    single rows and multiples of the 64-row tile), heads, batch, query set, K/V source,
+    segments (with random tile-aligned boundaries and cache flags) and key splits."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        d = int(rng.choice([64, 128]))
+        n_ref = int(rng.choice([0, 1, 63, 64, 65, int(rng.integers(2, 700))]))
+        n_tgt = int(rng.choice([1, 64, int(rng.integers(2, 500))]))
+        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+        qset = str(rng.choice(["target", "all"]))
+        kv = str(rng.choice(["fresh", "cache", "segments"])) if n_ref > 0 else "fresh"
+        segs, cached = None, None
+        if kv == "segments" or (n_ref > 64 and rng.random() < 0.3):
+            cuts = sorted(set(int(x) * 64 for x in rng.integers(1, max(2, (n_ref + 63) // 64), size=3)
+                              if int(x) * 64 < n_ref))
+            segs = cuts + [n_ref]
+            cached = [bool(x) for x in rng.integers(0, 2, size=len(segs))]
+        split = bool(rng.random() < 0.5)
+        cases.append((i, d, n_ref, n_tgt, B, H, qset, kv, segs, cached, split))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_cases(), ids=lambda c: f"r{c[0]}")
+def test_random_configurations_parity(case):
+    i, d, n_ref, n_tgt, B, H, qset, kv, segs, cached, split = case
+    print(f"random case {case}", flush=True)
+    _, x = _inputs("bf16", d, n_ref, n_tgt, B, H, seed=100 + i)
+    kw = {} if split else {"workspace": False}
+    if kv == "segments":
+        kr, vr, ends = _seg_oracle_inputs(x, np.diff([0] + segs).tolist(), cached)
+        kw.update(seg_end=ends, seg_cache=cached)
+    else:
+        use = kv == "cache"
+        kr = x["k_ref_cache"] if use else x["k_ref"]
+        vr = x["v_ref_cache"] if use else x["v_ref"]
+        if segs is not None:
+            kw.update(seg_end=segs)
+    want_seg = segs is not None
+    got = _gpu(x, "bf16", qset, kv, seg_mass=want_seg, **kw)
+    ref = joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"])
+    assert max_abs(host(got.o_tgt), ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["ref_mass"]) <= MASS_TOL["bf16"]
+    lse = host(got.lse)
+    assert max_abs(lse[..., 1], ref["lse_all"]) <= 1e-3
+    if n_ref > 0:
+        assert max_abs(lse[..., 0], ref["lse_ref"]) <= 1e-3
+    else:
+        assert np.all(np.isneginf(lse[..., 0]))
+    if want_seg:
+        assert max_abs(host(got.seg_mass), segment_masses(x["q_tgt"], kr, x["k_tgt"], segs)) <= MASS_TOL["bf16"]
+    if qset == "all" and n_ref > 0:
+        rr = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
+        assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]
+        assert max_abs(host(got.ref_mass_refq), rr["ref_mass"]) <= MASS_TOL["bf16"]
