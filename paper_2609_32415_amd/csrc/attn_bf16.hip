@@ -25,7 +25,9 @@
 // registers per lane each): while one wavefront forms probabilities the other
 // keeps the matrix core busy, and the eight wavefronts share every K/V tile
 // staged in LDS (two 16-byte chunks per thread per tile). Staging V only over
-// phase B keeps the register peak of phase A under that limit.
+// phase B keeps the register peak of phase A under that limit. s_setprio
+// alternates which wavefront of a SIMD wins issue ties between the phases, so
+// the pair finishes a tile together instead of one idling at the barrier.
 //
 // Online softmax in the exp2 domain without a per-tile row max: probabilities
 // are formed against the running max m, and a lane's partial row sum bounds
@@ -363,8 +365,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // partner gets the higher priority in phase A and the first one in phase B.
     const bool partner = __builtin_amdgcn_readfirstlane(wave) >= 4;
     if (partner) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
-    // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by a slice
-    // of the softmax of S_j: the row max, then the probabilities of P blocks 0 and 1.
+    // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by one pair of
+    // probabilities of S_j (pairs 0..9: P blocks 0, 1 and half of block 2).
     // At the last iteration the K buffer holds no tile and S_{j+1} is discarded.
     const uint16_t* kb = kbuf[jb ^ 1];
     auto k_operand = [&](int i) {  // i = KS * mb + kk
