@@ -17,15 +17,15 @@
 // the 16 MFMAs of O += V_j^T P_j^T, under the first six of which the remaining
 // pairs 10..15 are formed (phase B). sched_barrier fences keep that
 // order, so the vector ALU works while the matrix core runs. K tiles run one
-// tile ahead of V tiles through two LDS buffers each, refilled from registers:
-// the next K tile is loaded at the top of the iteration, the next V tile at the
-// start of phase B, and both are stored after phase B; one barrier per tile.
+// tile ahead of V tiles through two LDS buffers each. At the top of iteration j
+// direct global-to-LDS loads (no staging registers, no LDS store instructions)
+// fill the buffers that held K_j and V_{j-1} with K_{j+2} and V_{j+1}; the
+// iteration's one barrier, after a wait for those loads, publishes them.
 //
 // One workgroup fills a CU with two wavefronts per SIMD (at most 256 vector
 // registers per lane each): while one wavefront forms probabilities the other
 // keeps the matrix core busy, and the eight wavefronts share every K/V tile
-// staged in LDS (two 16-byte chunks per thread per tile). Staging V only over
-// phase B keeps the register peak of phase A under that limit. s_setprio
+// in LDS (each wavefront loads two 1 KiB blocks of each tile). s_setprio
 // alternates which wavefront of a SIMD wins issue ties between the phases, so
 // the pair finishes a tile together instead of one idling at the barrier.
 //
@@ -60,6 +60,7 @@
 #include <stdint.h>
 
 #include <atomic>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -102,32 +103,29 @@ __device__ __forceinline__ void pin(T& v) {
   asm volatile("" : "+v"(v));
 }
 
-// LDS layouts (bf16 elements):
-//   K tile: BN rows of stride D + 8 (row padding of 16 bytes); key r lives in LDS
-//           row sigma(r % 32) + 32 * (r / 32), so A-row m of an S^T block reads
-//           LDS row m. The 16-byte operand reads of 8 consecutive rows then hit
-//           8 distinct bank groups.
-//   V tile: BN rows of stride D + 32 (row padding of 64 bytes): keys of opposite
-//           parity fall in opposite bank halves, which makes the transpose reads
-//           of the V^T operand conflict-free.
+// LDS tiles are filled by direct global-to-LDS loads (buffer_load_dwordx4 ... lds):
+// one wavefront instruction writes 64 lanes x 16 bytes = one contiguous 1 KiB block,
+// lane L at byte 16 L. Each tile is D / 8 such blocks, and the lanes' global
+// addresses decide what lands where (bf16 elements; b(x, k) = bit k of x):
+//   K block kb = KS * mb + kk: 32 LDS rows n of 32 bytes, holding key 32 mb + sigma(n)
+//     and head dims 16 kk .. 16 kk + 15; chunk g (dims 16 kk + 8 g .. + 7) sits at
+//     byte 32 n + 16 (g ^ b(n, 3)). A-row n of an S^T block is LDS row n, and the 16
+//     lanes of one read phase hit 16 distinct 16-byte bank groups.
+//   V block vb = DB * s2 + db: 16 rows r of 64 bytes, holding key 16 s2 + r and head
+//     dims 32 db .. 32 db + 31, with the dim offset XORed by 16 when b(r, 1) is set,
+//     which makes the transpose reads of the V^T operand conflict-free.
+// No padding, no staging registers and no LDS store instructions: a tile's loads are
+// issued a whole iteration before the barrier that publishes it.
 template <int D>
 struct Layout {
-  static constexpr int KROW = D + 8;
-  static constexpr int VROW = D + 32;
-  static constexpr int KTILE = BN * KROW;
-  static constexpr int VTILE = BN * VROW;
-  static constexpr int KCH = D / 8;          // 16-byte chunks per row
-  static constexpr int NCH = BN * KCH / NT;  // chunks per thread per tile
+  static constexpr int NB = D / 8;        // 1 KiB blocks per K or V tile
+  static constexpr int TILE = NB * 512;   // elements per tile
+  static constexpr int NLD = NB / 8;      // blocks each of the 8 wavefronts loads per tile
 };
 
-template <int D>
-struct Staging {
-  u32x4 r[Layout<D>::NCH];
-};
-
-// Buffer resource of one K or V tile: base = its first row, range = its valid
-// rows, so loads of rows past a ragged tile's end return zero without a branch.
-// The base and range are workgroup-uniform; readfirstlane states it, so the
+// Buffer resource of one K or V tile: base = its first row, range = its valid rows, so
+// rows past a ragged tile's end load as zero (the range check covers the scalar offset
+// too). The base and range are workgroup-uniform; readfirstlane states it, so the
 // resource lives in scalar registers.
 template <int D>
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base, int64_t ss, int valid) {
@@ -139,23 +137,27 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t* base
   return __builtin_amdgcn_make_buffer_rsrc(ub, (short)0, (int)nbytes, 0x00020000);
 }
 
-// Thread t loads 16-byte chunk t % KCH of rows t / KCH + i * (NT / KCH): one
-// per-thread byte offset plus a uniform row step.
-template <int D>
-__device__ __forceinline__ void stage_load(Staging<D>& st, __amdgpu_buffer_rsrc_t rs, uint32_t voff, uint32_t step) {
-#pragma unroll
-  for (int i = 0; i < Layout<D>::NCH; ++i)
-    st.r[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff, __builtin_amdgcn_readfirstlane(i * step), 0);
+// Per-lane byte offset of the direct loads (row part with row stride ss elements, plus
+// the lane's 16-byte chunk); each block adds a uniform row and column offset.
+template <bool IS_K>
+__device__ __forceinline__ uint32_t dma_lane_offset(int lane, int64_t ss) {
+  if (IS_K) return (uint32_t)(sigma(lane >> 1) * ss * 2 + 16 * ((lane & 1) ^ ((lane >> 4) & 1)));
+  return (uint32_t)((lane >> 2) * ss * 2 + 16 * ((lane & 3) ^ (((lane >> 3) & 1) << 1)));
 }
 
-// The matching LDS stores: element offset of the thread's first chunk, then a
-// fixed row step (NT / KCH rows, which sigma leaves in place).
+// This wavefront's blocks of one K or V tile, straight into the LDS tile.
 template <int D, bool IS_K>
-__device__ __forceinline__ void stage_store(const Staging<D>& st, uint16_t* tile, int lds_off) {
-  constexpr int ROW = IS_K ? Layout<D>::KROW : Layout<D>::VROW;
-  constexpr int STEP = (NT / Layout<D>::KCH) * ROW;
+__device__ __forceinline__ void tile_dma(uint16_t* tile, __amdgpu_buffer_rsrc_t rs, uint32_t voff, int64_t ss,
+                                         int wave) {
+  constexpr int KS = D / 16, DB = D / 32;
 #pragma unroll
-  for (int i = 0; i < Layout<D>::NCH; ++i) *reinterpret_cast<u32x4*>(tile + lds_off + i * STEP) = st.r[i];
+  for (int i = 0; i < Layout<D>::NLD; ++i) {
+    const int blk = wave + 8 * i;
+    const int64_t soff = IS_K ? (int64_t)(blk / KS) * 32 * ss * 2 + (blk % KS) * 32
+                              : (int64_t)(blk / DB) * 16 * ss * 2 + (blk % DB) * 64;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(tile + blk * 512), 16,
+                                             voff, __builtin_amdgcn_readfirstlane((uint32_t)soff), 0, 0);
+  }
 }
 
 // SEG: reference segments: each reference key tile reads the fresh or the cached K/V of its
@@ -166,9 +168,13 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int DB = D / 32;   // 32-row blocks of the O^T accumulator
   constexpr int NQK = 2 * KS;  // MFMAs of one S^T tile
   constexpr int NPV = 4 * DB;  // MFMAs of one PV tile
-  constexpr int KROW = Layout<D>::KROW, VROW = Layout<D>::VROW;
-  __shared__ __attribute__((aligned(16))) uint16_t kbuf[2][Layout<D>::KTILE];
-  __shared__ __attribute__((aligned(16))) uint16_t vbuf[2][Layout<D>::VTILE];
+  // Four separate arrays (not one indexed by a run-time buffer number), so the compiler
+  // can tell the buffer a direct load fills from the ones being read and does not wait
+  // for the load before those reads.
+  __shared__ __attribute__((aligned(1024))) uint16_t kbuf0[Layout<D>::TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t kbuf1[Layout<D>::TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t vbuf0[Layout<D>::TILE];
+  __shared__ __attribute__((aligned(1024))) uint16_t vbuf1[Layout<D>::TILE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -219,16 +225,13 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   int64_t kr_ss = krv.ss, vr_ss = vrv.ss, ky_ss = p.k_tgt.ss, vy_ss = p.v_tgt.ss;
 
   auto tile_valid = [&](int j) { return j < n_rt ? min(BN, p.n_ref - j * BN) : min(BN, p.n_tgt - (j - n_rt) * BN); };
-  // Per-thread staging offsets (bytes into a tile, per segment) and LDS offsets.
-  constexpr int KCH = Layout<D>::KCH;
-  const int st_row = tid / KCH, st_ch = tid % KCH;
-  const uint32_t voff_r = (uint32_t)(st_row * krv.ss * 2 + st_ch * 16);
-  const uint32_t voff_rv = (uint32_t)(st_row * vrv.ss * 2 + st_ch * 16);
-  const uint32_t voff_yk = (uint32_t)(st_row * p.k_tgt.ss * 2 + st_ch * 16);
-  const uint32_t voff_yv = (uint32_t)(st_row * p.v_tgt.ss * 2 + st_ch * 16);
-  constexpr int ROWS_PER_STEP = NT / KCH;
-  const int k_st = ((st_row & ~31) | sigma(st_row & 31)) * KROW + st_ch * 8;
-  const int v_st = st_row * VROW + st_ch * 8;
+  // Per-lane byte offsets of the direct loads, per source view (the segments of SEG share
+  // the reference views' strides).
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t voff_r = dma_lane_offset<true>(lane, krv.ss);
+  const uint32_t voff_rv = dma_lane_offset<false>(lane, vrv.ss);
+  const uint32_t voff_yk = dma_lane_offset<true>(lane, p.k_tgt.ss);
+  const uint32_t voff_yv = dma_lane_offset<false>(lane, p.v_tgt.ss);
   // SEG: each of the K and V streams visits reference tiles in increasing order, so it keeps
   // its current segment and that segment's end tile, and reads a segment end from the
   // kernel arguments only when it crosses one.
@@ -242,48 +245,44 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     kbase = static_cast<const uint16_t*>(p.seg_kbase[0]) + kbh;
     vbase = static_cast<const uint16_t*>(p.seg_vbase[0]) + vbh;
   }
-  // Stages reference tile j of one of K, V (strides ss, lane offset voff) from the base of
-  // its segment.
-  auto load_ref_seg = [&](Staging<D>& st, int j, int& seg, int& end, const uint16_t*& base,
+  // Loads reference tile j of one of K, V (strides ss, lane offset voff) from the base of
+  // its segment into an LDS tile.
+  auto load_ref_seg = [&](auto is_k, uint16_t* dst, int j, int& seg, int& end, const uint16_t*& base,
                           const void* const* seg_base, int64_t bh_off, int64_t ss, uint32_t voff) {
     while (j >= end && seg + 1 < p.n_seg) {
       end = p.seg_tile_end[++seg];
       base = static_cast<const uint16_t*>(seg_base[seg]) + bh_off;
     }
-    stage_load<D>(st, tile_rsrc<D>(base + (int64_t)j * BN * ss, ss, tile_valid(j)), voff,
-                  (uint32_t)(ROWS_PER_STEP * ss * 2));
+    tile_dma<D, decltype(is_k)::value>(dst, tile_rsrc<D>(base + (int64_t)j * BN * ss, ss, tile_valid(j)), voff, ss,
+                                       wave_u);
   };
-  auto load_k = [&](Staging<D>& st, int j) {
+  auto load_k = [&](uint16_t* dst, int j) {
     const int valid = tile_valid(j);
     if constexpr (SEG) {
       if (j < n_rt) {
-        load_ref_seg(st, j, kseg, kend, kbase, p.seg_kbase, kbh, krv.ss, voff_r);
+        load_ref_seg(std::true_type{}, dst, j, kseg, kend, kbase, p.seg_kbase, kbh, krv.ss, voff_r);
         return;
       }
     }
-    if (j < n_rt) {
-      stage_load<D>(st, tile_rsrc<D>(kr + (int64_t)j * BN * kr_ss, kr_ss, valid), voff_r,
-                    (uint32_t)(ROWS_PER_STEP * kr_ss * 2));
-    } else {
-      stage_load<D>(st, tile_rsrc<D>(ky + (int64_t)(j - n_rt) * BN * ky_ss, ky_ss, valid), voff_yk,
-                    (uint32_t)(ROWS_PER_STEP * ky_ss * 2));
-    }
+    if (j < n_rt)
+      tile_dma<D, true>(dst, tile_rsrc<D>(kr + (int64_t)j * BN * kr_ss, kr_ss, valid), voff_r, kr_ss, wave_u);
+    else
+      tile_dma<D, true>(dst, tile_rsrc<D>(ky + (int64_t)(j - n_rt) * BN * ky_ss, ky_ss, valid), voff_yk, ky_ss,
+                        wave_u);
   };
-  auto load_v = [&](Staging<D>& st, int j) {
+  auto load_v = [&](uint16_t* dst, int j) {
     const int valid = tile_valid(j);
     if constexpr (SEG) {
       if (j < n_rt) {
-        load_ref_seg(st, j, vseg, vend, vbase, p.seg_vbase, vbh, vrv.ss, voff_rv);
+        load_ref_seg(std::false_type{}, dst, j, vseg, vend, vbase, p.seg_vbase, vbh, vrv.ss, voff_rv);
         return;
       }
     }
-    if (j < n_rt) {
-      stage_load<D>(st, tile_rsrc<D>(vr + (int64_t)j * BN * vr_ss, vr_ss, valid), voff_rv,
-                    (uint32_t)(ROWS_PER_STEP * vr_ss * 2));
-    } else {
-      stage_load<D>(st, tile_rsrc<D>(vy + (int64_t)(j - n_rt) * BN * vy_ss, vy_ss, valid), voff_yv,
-                    (uint32_t)(ROWS_PER_STEP * vy_ss * 2));
-    }
+    if (j < n_rt)
+      tile_dma<D, false>(dst, tile_rsrc<D>(vr + (int64_t)j * BN * vr_ss, vr_ss, valid), voff_rv, vr_ss, wave_u);
+    else
+      tile_dma<D, false>(dst, tile_rsrc<D>(vy + (int64_t)(j - n_rt) * BN * vy_ss, vy_ss, valid), voff_yv, vy_ss,
+                         wave_u);
   };
 
   // ---- this lane's query row; Q^T as the B operand (query n, head-dim chunk 2*kk + g)
@@ -300,21 +299,15 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
 
   // lane-dependent parts of the LDS operand addresses (everything else is an immediate)
-  const int k_lane = n * KROW + 8 * g;           // A-row n, head-dim chunk g
-  const int tr_i = lane & 15, tr_G = lane >> 4;  // 16-lane group of the transpose read
-  const int v_lane = (8 * (tr_G >> 1) + (tr_i >> 2)) * VROW + 16 * (tr_G & 1) + 4 * (tr_i & 3);
+  const int k_lane = 16 * n + 8 * (g ^ ((n >> 3) & 1));  // A-row n, head-dim chunk g
+  const int tr_i = lane & 15, tr_G = lane >> 4;         // 16-lane group of the transpose read
+  const int v_lane = 32 * (8 * (tr_G >> 1) + (tr_i >> 2)) + ((16 * (tr_G & 1) + 4 * (tr_i & 3)) ^ (16 * ((tr_i >> 3) & 1)));
 
   // ---- prologue: K_{j0}, K_{j0+1} and V_{j0} into LDS; S_{j0}. Tile j lives in
   // buffer (j - j0) & 1.
-  Staging<D> stk, stv;
-  load_k(stk, j0);
-  load_v(stv, j0);
-  stage_store<D, true>(stk, kbuf[0], k_st);
-  stage_store<D, false>(stv, vbuf[0], v_st);
-  if (j0 + 1 < j1) {
-    load_k(stk, j0 + 1);
-    stage_store<D, true>(stk, kbuf[1], k_st);
-  }
+  load_k(kbuf0, j0);
+  load_v(vbuf0, j0);
+  if (j0 + 1 < j1) load_k(kbuf1, j0 + 1);
   __syncthreads();
   f32x16 sa[2], sb[2];
 #pragma unroll
@@ -322,7 +315,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     sa[mb] = f32x16{};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbuf[0] + k_lane + 32 * mb * KROW + 16 * kk);
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(kbuf0 + k_lane + 512 * (KS * mb + kk));
       sa[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sa[mb], 0, 0, 0);
     }
   }
@@ -338,8 +331,9 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   int seg_idx = 0, seg_end_t = SEG && n_rt > 0 ? p.seg_tile_end[0] : -1;
   const int64_t seg_row = ((int64_t)bh * p.n_tgt + qrow) * p.n_seg;
 
-  auto iteration = [&](int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
-    const int jb = (j - j0) & 1;  // LDS buffer of K_j and V_j
+  // jbc: the LDS buffer of K_j and V_j, (j - j0) & 1, as a compile-time constant.
+  auto iteration = [&](auto jbc, int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
+    constexpr int jb = decltype(jbc)::value;
     // Keep the per-workgroup tile sources in registers: rematerialising them from the kernel
     // arguments would put a scalar load under the first MFMA's LDS wait.
     asm volatile("" : "+s"(kr), "+s"(vr), "+s"(ky), "+s"(vy));
@@ -347,7 +341,12 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // Global loads for the tiles this iteration stages: K_{j+2} here, V_{j+1} at the
     // start of phase B. Past the workgroup's last key tile the index is clamped to
     // it: the reload lands in a buffer that is never read again.
-    load_k(stk, min(j + 2, j1 - 1));
+    uint16_t* const kb_cur = jb ? kbuf1 : kbuf0;   // K_j (already read), refilled with K_{j+2}
+    uint16_t* const kb_next = jb ? kbuf0 : kbuf1;  // K_{j+1}
+    uint16_t* const vb_cur = jb ? vbuf1 : vbuf0;   // V_j
+    uint16_t* const vb_next = jb ? vbuf0 : vbuf1;  // V_{j-1} (already read), refilled with V_{j+1}
+    load_k(kb_cur, min(j + 2, j1 - 1));
+    load_v(vb_next, min(j + 1, j1 - 1));
 
     const int valid = tile_valid(j);
     if (valid < BN) {  // ragged last tile of a segment: drop keys past its end
@@ -368,9 +367,9 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by one pair of
     // probabilities of S_j (pairs 0..9: P blocks 0, 1 and half of block 2).
     // At the last iteration the K buffer holds no tile and S_{j+1} is discarded.
-    const uint16_t* kb = kbuf[jb ^ 1];
+    const uint16_t* kb = kb_next;
     auto k_operand = [&](int i) {  // i = KS * mb + kk
-      return *reinterpret_cast<const bf16x8*>(kb + k_lane + 32 * (i / KS) * KROW + 16 * (i % KS));
+      return *reinterpret_cast<const bf16x8*>(kb + k_lane + 512 * i);
     };
     uint32_t pw[4][4];  // packed bf16 probabilities: P block s2, keys 16*s2 + 8*g + 2w, +1
     // Row-sum chains: pairs 0..7 (P blocks 0, 1) and pairs 8..15 (P blocks 2, 3).
@@ -442,12 +441,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // 2 and 3 are formed under the MFMAs of blocks 0 and 1. V^T operands come from
     // LDS transpose reads issued two MFMAs ahead.
     if (partner) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
-    load_v(stv, min(j + 1, j1 - 1));
-    const uint16_t* vs = vbuf[jb];
+    const uint16_t* vs = vb_cur;
     auto v_operand = [&](int i) {  // i = DB * s2 + db
-      const uint16_t* a = vs + v_lane + 16 * (i / DB) * VROW + 32 * (i % DB);
+      const uint16_t* a = vs + v_lane + 512 * i;
       const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(a));
-      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(a + 4 * VROW));
+      const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(a + 128));
       return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     };
     bf16x8 va[3];
@@ -503,17 +501,15 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       l_ref = l_run;
       l_run = 0.f;
     }
-    stage_store<D, true>(stk, kbuf[jb], k_st);
-    stage_store<D, false>(stv, vbuf[jb ^ 1], v_st);
     __syncthreads();
   };
 
   int j = j0;
   for (; j + 1 < j1; j += 2) {
-    iteration(j, sa, sb);
-    iteration(j + 1, sb, sa);
+    iteration(std::integral_constant<int, 0>{}, j, sa, sb);
+    iteration(std::integral_constant<int, 1>{}, j + 1, sb, sa);
   }
-  if (j < j1) iteration(j, sa, sb);
+  if (j < j1) iteration(std::integral_constant<int, 0>{}, j, sa, sb);
   if (j1 < n_rt) {  // a key chunk inside the reference segment: all of it is reference mass
     m_ref = m_run;
     l_ref = l_run;
