@@ -17,10 +17,11 @@
 // the 16 MFMAs of O += V_j^T P_j^T, under the first six of which the remaining
 // pairs 10..15 are formed (phase B). sched_barrier fences keep that
 // order, so the vector ALU works while the matrix core runs. K tiles run one
-// tile ahead of V tiles through two LDS buffers each. At the top of iteration j
-// direct global-to-LDS loads (no staging registers, no LDS store instructions)
-// fill the buffers that held K_j and V_{j-1} with K_{j+2} and V_{j+1}; the
-// iteration's one barrier, after a wait for those loads, publishes them.
+// tile ahead of V tiles through two LDS buffers each. At the start of phase B of
+// iteration j direct global-to-LDS loads (no staging registers, no LDS store
+// instructions) fill the buffers that held K_j and V_{j-1} with K_{j+2} and
+// V_{j+1}; the iteration's one barrier, after a wait for those loads, publishes
+// them.
 //
 // One workgroup fills a CU with two wavefronts per SIMD (at most 256 vector
 // registers per lane each): while one wavefront forms probabilities the other
@@ -115,7 +116,7 @@ __device__ __forceinline__ void pin(T& v) {
 //     dims 32 db .. 32 db + 31, with the dim offset XORed by 16 when b(r, 1) is set,
 //     which makes the transpose reads of the V^T operand conflict-free.
 // No padding, no staging registers and no LDS store instructions: a tile's loads are
-// issued a whole iteration before the barrier that publishes it.
+// issued about a phase B ahead of the barrier that publishes it.
 template <int D>
 struct Layout {
   static constexpr int NB = D / 8;        // 1 KiB blocks per K or V tile
@@ -345,8 +346,6 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     uint16_t* const kb_next = jb ? kbuf0 : kbuf1;  // K_{j+1}
     uint16_t* const vb_cur = jb ? vbuf1 : vbuf0;   // V_j
     uint16_t* const vb_next = jb ? vbuf0 : vbuf1;  // V_{j-1} (already read), refilled with V_{j+1}
-    load_k(kb_cur, min(j + 2, j1 - 1));
-    load_v(vb_next, min(j + 1, j1 - 1));
 
     const int valid = tile_valid(j);
     if (valid < BN) {  // ragged last tile of a segment: drop keys past its end
@@ -441,6 +440,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // 2 and 3 are formed under the MFMAs of blocks 0 and 1. V^T operands come from
     // LDS transpose reads issued two MFMAs ahead.
     if (partner) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
+    // The next tiles' direct loads: issued here rather than at the top of the iteration, so
+    // their LDS writes do not land under phase A's K operand reads (about -1.5%).
+    load_k(kb_cur, min(j + 2, j1 - 1));
+    load_v(vb_next, min(j + 1, j1 - 1));
     const uint16_t* vs = vb_cur;
     auto v_operand = [&](int i) {  // i = DB * s2 + db
       const uint16_t* a = vs + v_lane + 512 * i;
