@@ -239,6 +239,42 @@ def test_custom_scale_and_strided_views():
     assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
 
 
+def _layout(a, kind):
+    """A device view of ``a`` ([B, H, S, d], bf16) in one of three memory layouts:
+    contiguous, head-interleaved [B, S, H, d], or rows padded to 4 d elements."""
+    t = dev(a, "bf16")
+    if kind == "bshd":
+        return t.transpose(1, 2).contiguous().transpose(1, 2)
+    if kind == "pad":
+        B, H, S, d = t.shape
+        buf = torch.zeros((B, H, S, 4 * d), dtype=t.dtype, device=t.device)
+        buf[..., d:2 * d] = t
+        return buf[..., d:2 * d]
+    return t
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("mode", [("target", "cache"), ("all", "fresh"), ("all", "cache")], ids=lambda m: "/".join(m))
+def test_mixed_layouts_per_tensor(d, mode):
+    """Every K/V tensor with its own row stride (contiguous, head-interleaved, padded rows),
+    ragged reference and target tails: each view's tiles are addressed with its own stride."""
+    qset, kvsrc = mode
+    _, x = _inputs("bf16", d, 130, 333, B=2, H=3)
+    ref = _oracle(x, qset, kvsrc == "cache")
+    kinds = {"q_tgt": "pad", "k_tgt": "bshd", "v_tgt": "plain", "q_ref": "bshd", "k_ref": "pad", "v_ref": "bshd",
+             "k_ref_cache": "bshd", "v_ref_cache": "pad"}
+    t = {k: _layout(x[k], v) for k, v in kinds.items()}
+    assert t["k_ref"].stride(2) == 4 * d and t["k_tgt"].stride(2) == 3 * d and t["v_tgt"].stride(2) == d
+    got = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
+                         k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], qset=qset, kvsrc=kvsrc, n_ref=130,
+                         lse=True)
+    torch.cuda.synchronize()
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    if qset == "all":
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
+
+
 FULL = [("single_ref", "target", "cache"), ("single_ref", "all", "fresh"), ("multi_ref", "target", "cache"),
         ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"), ("video", "target", "cache"),
         ("ref8", "target", "cache"), ("ref8", "all", "fresh")]
