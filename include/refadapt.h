@@ -168,7 +168,8 @@ typedef struct {
  * segment ends that do not increase to n_ref). RA_EUNSUPPORTED for head_dim not
  * in {64, 128} or misaligned tensors or workspace, and for segments with
  * RA_F32, RA_KV_DEVICE, an inner boundary off the 64-row key tiles, or (under
- * RA_KV_SEGMENTS) fresh and cached views with different strides. RA_EWORKSPACE for a
+ * RA_KV_SEGMENTS) fresh and cached views with different strides, and (RA_BF16) for a
+ * K/V row stride above 2^24 - 8 elements (key tiles use 32-bit offsets). RA_EWORKSPACE for a
  * non-NULL workspace smaller than refadapt_joint_attn_workspace_size(desc).
  */
 ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream);

@@ -224,6 +224,16 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
     if ((s = check_tensor("o_ref", a.o_ref, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
   }
   if (device && a.decision == nullptr) return fail(RA_EINVAL, "joint_attn: RA_KV_DEVICE needs a decision pointer");
+  if (d.dtype == RA_BF16) {
+    // K/V tiles are addressed with 32-bit buffer offsets: 64 rows of the row stride must fit.
+    const ra_tensor* kv[] = {&a.k_tgt, &a.v_tgt, &a.k_ref, &a.v_ref, &a.k_cache, &a.v_cache};
+    const char* kv_name[] = {"k_tgt", "v_tgt", "k_ref", "v_ref", "k_cache", "v_cache"};
+    const bool used[] = {true, true, reads_fresh, reads_fresh, reads_cache, reads_cache};
+    for (int i = 0; i < 6; ++i)
+      if (used[i] && kv[i]->stride_s > kAttnMaxRowStride)
+        return fail(RA_EUNSUPPORTED, "joint_attn: %s row stride %lld exceeds %lld elements", kv_name[i],
+                    (long long)kv[i]->stride_s, (long long)kAttnMaxRowStride);
+  }
   if (d.kvsrc == RA_KV_SEGMENTS && reads_fresh && reads_cache) {
     const auto same = [](const ra_tensor& x, const ra_tensor& y) {
       return x.stride_b == y.stride_b && x.stride_h == y.stride_h && x.stride_s == y.stride_s;

@@ -67,6 +67,9 @@ struct AttnParams {
 // these) and keys per key tile of the bf16 kernel.
 constexpr int kAttnBf16BM = 256;
 constexpr int kAttnBf16BN = 64;
+// Largest K/V row stride (elements) of the bf16 attention: a key tile spans 64 rows, addressed
+// with 32-bit byte offsets.
+constexpr int64_t kAttnMaxRowStride = (int64_t(1) << 24) - 8;
 constexpr int kAttnF32BM = 64;
 
 // Compute units of the current device and bf16 attention workgroups each holds

@@ -62,6 +62,7 @@ def _args(**kw):
         ({}, dict(q_tgt=_t(ss=132)), L.RA_EUNSUPPORTED, "q_tgt"),
         ({}, dict(v_tgt=_t(ptr=0x1002)), L.RA_EUNSUPPORTED, "v_tgt"),
         ({}, dict(k_tgt=_t(ss=64)), L.RA_EINVAL, "row stride"),
+        ({}, dict(v_ref=_t(ss=1 << 24)), L.RA_EUNSUPPORTED, "v_ref row stride"),
         (dict(batch=0), {}, L.RA_EINVAL, "batch"),
         ({}, dict(workspace=0x1008, workspace_bytes=1 << 20), L.RA_EUNSUPPORTED, "workspace"),
     ],
