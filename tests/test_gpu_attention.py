@@ -275,6 +275,36 @@ def test_mixed_layouts_per_tensor(d, mode):
         assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
 
 
+def _nan_padded(a, pad=64):
+    """A device view of ``a`` ([B, H, S, d], bf16) whose buffer holds ``pad`` NaN rows after the
+    S rows of every head: any load past a tensor's last row would poison the result."""
+    t = dev(a, "bf16")
+    B, H, S, d = t.shape
+    buf = torch.full((B, H, S + pad, d), float("nan"), dtype=t.dtype, device=t.device)
+    buf[:, :, :S] = t
+    return buf[:, :, :S]
+
+
+@pytest.mark.parametrize("d", [128, 64])
+@pytest.mark.parametrize("mode", [("target", "cache"), ("all", "fresh")], ids=lambda m: "/".join(m))
+def test_ragged_tiles_never_read_past_the_last_row(d, mode):
+    """Every K/V view sits in a buffer with NaN rows after its last row; ragged last tiles must
+    load those rows as zeros (buffer range check), so O, mass and lse stay finite and exact."""
+    qset, kvsrc = mode
+    _, x = _inputs("bf16", d, 130, 77, B=1, H=2)
+    ref = _oracle(x, qset, kvsrc == "cache")
+    t = {k: (_nan_padded(v) if k[0] in "kv" else dev(v, "bf16")) for k, v in x.items()}
+    got = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
+                         k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], qset=qset, kvsrc=kvsrc, n_ref=130,
+                         lse=True, workspace=False)
+    torch.cuda.synchronize()
+    assert np.isfinite(host(got.o_tgt)).all() and np.isfinite(host(got.lse)).all()
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    if qset == "all":
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
+
+
 FULL = [("single_ref", "target", "cache"), ("single_ref", "all", "fresh"), ("multi_ref", "target", "cache"),
         ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"), ("video", "target", "cache"),
         ("ref8", "target", "cache"), ("ref8", "all", "fresh")]
