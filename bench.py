@@ -21,7 +21,8 @@ stream, and the fp64 CPU oracle timed on a bounded sample of the same work.
 (single-reference shapes, 3 x 3 thresholds, cue ablation, graph replays) and
 reports the reuse fraction, the attention-time speedup of adaptive reuse and
 the output error against a full-fresh trajectory. ``--ref-sweep`` runs the
-reference-count sweep (1..8 reference images).
+reference-count sweep (1..8 reference images). ``--shapes`` times the reuse and
+full-fresh attention at the single-reference, multi-reference and video shapes.
 """
 
 from __future__ import annotations
@@ -54,7 +55,9 @@ def parse_args():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # ~55 ms of steps: after the host-side input generation the GPU clock needs tens of
+    # milliseconds of load to come back up
+    ap.add_argument("--warmup", type=int, default=15)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target duration of the oracle sample")
     ap.add_argument("--sweep", action="store_true", help="also run the 60-block x 8-step controller sweep")
@@ -64,6 +67,8 @@ def parse_args():
                     help="also run the per-reference exposure / individual stale impact table")
     ap.add_argument("--ref-sweep", action="store_true",
                     help="also run the reference-count sweep (1..8 reference images at single-reference shapes)")
+    ap.add_argument("--shapes", action="store_true",
+                    help="also time the reuse and full-fresh attention at the single-reference, multi-reference and video shapes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the cache-commit copy over 2 x 512 MiB (a plain copy of known size, "
                     "for scaling the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -99,6 +104,46 @@ def _traffic_from_profile():
         return None
     cur = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
     return float(m_b.group(1)) if cur == m_src.group(1) else None
+
+
+def time_shapes(dev, reps=10):
+    """Reuse (target queries, cached K/V) and full-fresh (all queries, fresh K/V) attention at
+    the single-reference, multi-reference and video workload shapes, seeded synthetic inputs
+    (the fresh reference K/V stand in for the cache), event-timed over ``reps`` launches after
+    warm-up."""
+    import torch
+
+    from paper_2609_32415_amd import ops, synth
+    from paper_2609_32415_amd.controller import time_launches
+
+    rows = []
+    for name in ("single_ref", "multi_ref", "video"):
+        w = synth.workload(name)
+        x = synth.block_inputs(w)
+        bf = lambda a: torch.from_numpy(a).to(dev).to(torch.bfloat16)
+        t = {k: bf(x[k]) for k in ("q_tgt", "k_tgt", "v_tgt", "q_ref", "k_ref", "v_ref")}
+        B, H, n_tgt, D = t["q_tgt"].shape
+        n_ref = t["k_ref"].shape[2]
+        ws_r = ops.attn_workspace(t["q_tgt"], n_ref, "target", "cache")
+        ws_f = ops.attn_workspace(t["q_tgt"], n_ref, "all", "fresh")
+        calls = {
+            "reuse": (lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=t["k_ref"], v_cache=t["v_ref"],
+                                             n_ref=n_ref, qset="target", kvsrc="cache", workspace=ws_r),
+                      attn_flops(H, n_tgt, n_ref + n_tgt, D, B)),
+            "full_fresh": (lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"],
+                                                  v_ref=t["v_ref"], qset="all", kvsrc="fresh", workspace=ws_f),
+                           attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, D, B)),
+        }
+        row = {"workload": name, "heads": H, "head_dim": D, "n_ref": n_ref, "n_tgt": n_tgt}
+        for mode, (fn, flop) in calls.items():
+            ms = time_launches(fn, reps=reps)
+            tf = flop / (ms * 1e-3) / 1e12
+            row[mode] = {"ms": round(ms, 4), "tflops": round(tf, 2), "pct_peak": round(100 * tf / BF16_PEAK_TFLOPS, 2)}
+        rows.append(row)
+        print(f"shape {name}: reuse {row['reuse']}, full-fresh {row['full_fresh']}", file=sys.stderr, flush=True)
+        del t, x
+        torch.cuda.empty_cache()
+    return rows
 
 
 def cpu_baseline(x, seconds):
@@ -334,6 +379,8 @@ def main():
         from paper_2609_32415_amd.controller import run_reference_segments
 
         out["reference_segments"] = run_reference_segments(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+    if args.shapes:
+        out["shapes"] = time_shapes(dev)
     if args.ref_sweep:
         from paper_2609_32415_amd.controller import run_ref_count_sweep
 

@@ -245,6 +245,24 @@ def _sweep_inputs(w, device):
     return trajs
 
 
+def time_launches(fn, reps=10, warm_ms=50.0):
+    """Mean time (ms) of ``fn`` over ``reps`` back-to-back launches, after at least ``warm_ms`` of
+    warm-up launches: after host-side work the GPU clock needs tens of milliseconds of load to
+    come back up, and a short warm-up then times the ramp, not the kernel."""
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    fn()
+    b.record()
+    torch.cuda.synchronize()
+    for _ in range(max(5, int(warm_ms / max(a.elapsed_time(b), 1e-3)))):
+        fn()
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
 def _timed_run(w, device, theta, delta_max, mode="product", theta_m=None, keep=None, cue="consecutive",
                sidecar=None):
     """One trajectory; returns (controller, per-step attention-path milliseconds)."""
@@ -516,21 +534,9 @@ def run_ref_count_sweep(device="cuda:0", counts=(1, 2, 3, 4, 5, 6, 7, 8), n_bloc
         ws_r = ops.attn_workspace(x["q_tgt"], w.n_ref, "target", "cache")
         ws_f = ops.attn_workspace(x["q_tgt"], w.n_ref, "all", "fresh")
 
-        def timed(fn, n=10):
-            for _ in range(2):
-                fn()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            a.record()
-            for _ in range(n):
-                fn()
-            b.record()
-            torch.cuda.synchronize()
-            return a.elapsed_time(b) / n
-
-        t_reuse = timed(lambda: ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_cache=x["k_ref"],
+        t_reuse = time_launches(lambda: ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], k_cache=x["k_ref"],
                                                v_cache=x["v_ref"], n_ref=w.n_ref, kvsrc="cache", workspace=ws_r))
-        t_full = timed(lambda: ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"],
+        t_full = time_launches(lambda: ops.joint_attn(x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"],
                                               v_ref=x["v_ref"], qset="all", workspace=ws_f))
         del x, ws_r, ws_f
         _, base_ms = _timed_run(w, device, 0.0, delta_max=1)
@@ -608,17 +614,7 @@ def run_reference_segments(device="cuda:0", weights=(1.0, 0.5, 0.0, 1.0), sizes=
     order2 = [1, 0] + list(range(2, n_seg))
     ex2, im2, im_all2, _ = table(order2)
 
-    def timed(fn, n=20):
-        for _ in range(3):
-            fn()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(n):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / n
-
+    timed = lambda fn: time_launches(fn, reps=20)
     mixed = [i % 2 == 0 for i in range(n_seg)]
     ws = ops.attn_workspace(t["q_tgt"], sum(sizes), "target", "cache")
     ms_cache = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=kc, v_cache=vc,
