@@ -161,6 +161,50 @@ __device__ __forceinline__ void tile_dma(uint16_t* tile, __amdgpu_buffer_rsrc_t 
   }
 }
 
+// Direct-load cursor of one K or V stream: the next key tile to load, the first row of that
+// tile, the rows of its view from there on, and the view's row stride, lane offset and the
+// scalar offsets of this wavefront's blocks. Advancing to the next tile costs a 64-bit add;
+// the view changes once, where the reference keys end and the target keys begin.
+template <int D, bool IS_K>
+struct DmaCursor {
+  const uint16_t* ptr;
+  int64_t ss;
+  uint32_t voff;
+  uint32_t soff[Layout<D>::NLD];
+  int t, rows;
+
+  __device__ __forceinline__ void set_view(const uint16_t* base, int64_t row_stride, uint32_t lane_off, int tile0,
+                                           int first_row, int view_rows, int wave) {
+    constexpr int KS = D / 16, DB = D / 32;
+    ss = row_stride;
+    voff = lane_off;
+    ptr = base + (int64_t)first_row * ss;
+    rows = view_rows - first_row;
+    t = tile0;
+#pragma unroll
+    for (int i = 0; i < Layout<D>::NLD; ++i) {
+      const int blk = wave + 8 * i;
+      soff[i] = __builtin_amdgcn_readfirstlane(
+          (uint32_t)(IS_K ? (int64_t)(blk / KS) * 32 * ss * 2 + (blk % KS) * 32
+                          : (int64_t)(blk / DB) * 16 * ss * 2 + (blk % DB) * 64));
+    }
+  }
+  // loads tile t into `tile` and advances to tile t + 1
+  __device__ __forceinline__ void load(uint16_t* tile, int wave) {
+    const int valid = min(BN, rows);
+    const __amdgpu_buffer_rsrc_t rs = tile_rsrc<D>(ptr, ss, valid);
+#pragma unroll
+    for (int i = 0; i < Layout<D>::NLD; ++i) {
+      const int blk = wave + 8 * i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)(tile + blk * 512), 16,
+                                               voff, soff[i], 0, 0);
+    }
+    ptr += BN * ss;
+    rows -= BN;
+    t += 1;
+  }
+};
+
 // SEG: reference segments: each reference key tile reads the fresh or the cached K/V of its
 // segment; with seg_mass (whole tiles only) each segment's log-sum-exp is recorded.
 template <int D, bool SEG>
@@ -234,9 +278,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const uint32_t voff_yk = dma_lane_offset<true>(lane, p.k_tgt.ss);
   const uint32_t voff_yv = dma_lane_offset<false>(lane, p.v_tgt.ss);
   // SEG: each of the K and V streams visits reference tiles in increasing order, so it keeps
-  // its current segment and that segment's end tile, and reads a segment end from the
-  // kernel arguments only when it crosses one.
-  // The cursor keeps the segment's base pointer (this (b, h) applied) and end tile and
+  // its current segment, that segment's base pointer (this (b, h) applied) and end tile, and
   // reads the next ones from the kernel arguments only when it crosses a segment end.
   int kseg = 0, kend = 0, vseg = 0, vend = 0;
   const uint16_t *kbase = nullptr, *vbase = nullptr;
@@ -321,6 +363,20 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     }
   }
   __syncthreads();  // every wavefront has read K_{j0} before the first iteration refills its buffer
+  // cursors of the in-loop loads: K from tile j0 + 2, V from tile j0 + 1
+  DmaCursor<D, true> kc;
+  DmaCursor<D, false> vc;
+  auto cursor_view = [&](auto& cur, bool is_k, int tile) {
+    if (tile < n_rt)
+      cur.set_view(is_k ? kr : vr, is_k ? kr_ss : vr_ss, is_k ? voff_r : voff_rv, tile, tile * BN, p.n_ref, wave_u);
+    else
+      cur.set_view(is_k ? ky : vy, is_k ? ky_ss : vy_ss, is_k ? voff_yk : voff_yv, tile, (tile - n_rt) * BN, p.n_tgt,
+                   wave_u);
+  };
+  if constexpr (!SEG) {
+    cursor_view(kc, true, j0 + 2);
+    cursor_view(vc, false, j0 + 1);
+  }
 
   f32x16 o[DB];
 #pragma unroll
@@ -335,13 +391,16 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   // jbc: the LDS buffer of K_j and V_j, (j - j0) & 1, as a compile-time constant.
   auto iteration = [&](auto jbc, int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
     constexpr int jb = decltype(jbc)::value;
-    // Keep the per-workgroup tile sources in registers: rematerialising them from the kernel
-    // arguments would put a scalar load under the first MFMA's LDS wait.
-    asm volatile("" : "+s"(kr), "+s"(vr), "+s"(ky), "+s"(vy));
-    asm volatile("" : "+s"(kr_ss), "+s"(vr_ss), "+s"(ky_ss), "+s"(vy_ss));
-    // Global loads for the tiles this iteration stages: K_{j+2} here, V_{j+1} at the
-    // start of phase B. Past the workgroup's last key tile the index is clamped to
-    // it: the reload lands in a buffer that is never read again.
+    // Segment kernel: keep the per-workgroup tile sources in registers (rematerialising them
+    // from the kernel arguments would put a scalar load under the first MFMA's LDS wait). The
+    // other kernels address their loads through the K and V cursors instead.
+    if constexpr (SEG) {
+      asm volatile("" : "+s"(kr), "+s"(vr), "+s"(ky), "+s"(vy));
+      asm volatile("" : "+s"(kr_ss), "+s"(vr_ss), "+s"(ky_ss), "+s"(vy_ss));
+    }
+    // Global loads for the tiles this iteration stages: K_{j+2} and V_{j+1}, issued at the
+    // start of phase B. Past the workgroup's last key tile the segment kernel reloads that
+    // tile into a buffer that is never read again; the cursors skip the load.
     uint16_t* const kb_cur = jb ? kbuf1 : kbuf0;   // K_j (already read), refilled with K_{j+2}
     uint16_t* const kb_next = jb ? kbuf0 : kbuf1;  // K_{j+1}
     uint16_t* const vb_cur = jb ? vbuf1 : vbuf0;   // V_j
@@ -442,8 +501,19 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     if (partner) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
     // The next tiles' direct loads: issued here rather than at the top of the iteration, so
     // their LDS writes do not land under phase A's K operand reads (about -1.5%).
-    load_k(kb_cur, min(j + 2, j1 - 1));
-    load_v(vb_next, min(j + 1, j1 - 1));
+    if constexpr (SEG) {
+      load_k(kb_cur, min(j + 2, j1 - 1));
+      load_v(vb_next, min(j + 1, j1 - 1));
+    } else {
+      if (kc.t < j1) {
+        if (kc.t == n_rt) cursor_view(kc, true, kc.t);
+        kc.load(kb_cur, wave_u);
+      }
+      if (vc.t < j1) {
+        if (vc.t == n_rt) cursor_view(vc, false, vc.t);
+        vc.load(vb_next, wave_u);
+      }
+    }
     const uint16_t* vs = vb_cur;
     auto v_operand = [&](int i) {  // i = DB * s2 + db
       const uint16_t* a = vs + v_lane + 512 * i;
