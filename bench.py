@@ -188,7 +188,7 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(
-            "bench.py measures one MI355X: the hot path has no multi-GPU leg in this build "
+            "bench.py measures one MI355X: the hot path has no multi-GPU leg "
             "(heads would shard across GPUs with one head-mean all-reduce per gated block). "
             "Run with --gpus 1.",
             file=sys.stderr,

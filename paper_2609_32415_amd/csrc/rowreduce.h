@@ -17,6 +17,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int QC_THREADS = 256;
 constexpr int QC_TARGET_ELEMS = 16384;  // elements of one tensor per workgroup (32 KiB of bf16)
 constexpr int QC_MAX_CHUNKS = 64;
+constexpr int QC_UNROLL = 4;  // 16-byte vectors of each tensor per thread in flight
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -42,28 +43,43 @@ __device__ __forceinline__ float2 q_change_rows(View cur, View prev, int b, int 
   const int64_t pbase = (b * prev.sb + h * prev.sh) * esz;
 
   float sd = 0.f, sp = 0.f;
-  for (int v = threadIdx.x; v < nvec; v += QC_THREADS) {
-    const int row = r0 + v / vpr, col = (v % vpr) * vec;
-    const u32x4 x = *reinterpret_cast<const u32x4*>(cb + cbase + ((int64_t)row * cur.ss + col) * esz);
-    const u32x4 y = *reinterpret_cast<const u32x4*>(pb + pbase + ((int64_t)row * prev.ss + col) * esz);
-    if (BF16) {
+  // QC_UNROLL vectors of each tensor are loaded before any is used, so each thread keeps
+  // 2 * QC_UNROLL loads in flight. Vectors past the end load as zeros, which add exactly
+  // +0 to both sums: the per-thread order is the plain strided order.
+  for (int v0 = threadIdx.x; v0 < nvec; v0 += QC_UNROLL * QC_THREADS) {
+    u32x4 xs[QC_UNROLL], ys[QC_UNROLL];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float a0 = bf16_lo(x[i]), a1 = bf16_hi(x[i]);
-        const float p0 = bf16_lo(y[i]), p1 = bf16_hi(y[i]);
-        const float d0 = a0 - p0, d1 = a1 - p1;
-        sd = fmaf(d0, d0, sd);
-        sd = fmaf(d1, d1, sd);
-        sp = fmaf(p0, p0, sp);
-        sp = fmaf(p1, p1, sp);
+    for (int u = 0; u < QC_UNROLL; ++u) {
+      const int v = v0 + u * QC_THREADS;
+      xs[u] = ys[u] = u32x4{0u, 0u, 0u, 0u};
+      if (v < nvec) {
+        const int row = r0 + v / vpr, col = (v % vpr) * vec;
+        xs[u] = *reinterpret_cast<const u32x4*>(cb + cbase + ((int64_t)row * cur.ss + col) * esz);
+        ys[u] = *reinterpret_cast<const u32x4*>(pb + pbase + ((int64_t)row * prev.ss + col) * esz);
       }
-    } else {
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float a = __uint_as_float(x[i]), pp = __uint_as_float(y[i]);
-        const float d = a - pp;
-        sd = fmaf(d, d, sd);
-        sp = fmaf(pp, pp, sp);
+    for (int u = 0; u < QC_UNROLL; ++u) {
+      const u32x4 x = xs[u], y = ys[u];
+      if (BF16) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float a0 = bf16_lo(x[i]), a1 = bf16_hi(x[i]);
+          const float p0 = bf16_lo(y[i]), p1 = bf16_hi(y[i]);
+          const float d0 = a0 - p0, d1 = a1 - p1;
+          sd = fmaf(d0, d0, sd);
+          sd = fmaf(d1, d1, sd);
+          sp = fmaf(p0, p0, sp);
+          sp = fmaf(p1, p1, sp);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float a = __uint_as_float(x[i]), pp = __uint_as_float(y[i]);
+          const float d = a - pp;
+          sd = fmaf(d, d, sd);
+          sp = fmaf(pp, pp, sp);
+        }
       }
     }
   }
