@@ -272,21 +272,56 @@ def main():
     ms = {k: float(np.mean(v)) for k, v in marks.items()}
     ms_per_step = total_ms / args.steps
 
-    # Outside the timed step: the separate Q-change and gate kernels the fused launch replaces.
+    # Outside the timed step: the separate Q-change and gate kernels the fused launch replaces,
+    # and the diagnostics. Two figures each:
+    #  * cold: one launch between events after a 512 MiB read (a reduction, so no dirty lines
+    #    are left to write back) has evicted its inputs from the 256 MB last-level cache;
+    #  * hot: n back-to-back launches replayed from a captured HIP graph (device time per
+    #    launch with the inputs cache-resident; no host launch gaps).
+    flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+
     def timed(fn, n=20):
         for _ in range(3):
             fn()
+        pairs = []
+        for _ in range(n):
+            flush.sum()
+            a, b = ev(), ev()
+            a.record()
+            fn()
+            b.record()
+            pairs.append((a, b))
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+
+    def timed_hot(fn, n=20):
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(n):
+                fn()
+        for _ in range(3):
+            g.replay()
         a, b = ev(), ev()
         a.record()
-        for _ in range(n):
-            fn()
+        g.replay()
         b.record()
         torch.cuda.synchronize()
         return a.elapsed_time(b) / n
 
-    ms["qc"] = timed(lambda: ops.q_change(t["q_tgt"], q_prev, out=d_out, workspace=ws))
-    ms["gate"] = timed(lambda: ops.gate(d_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec,
-                                        score_out=score))
+    def qcg():
+        ops.q_change_gate(t["q_tgt"], q_prev, mass_prev, theta, state, 0, 1, "product", d_out=d_out,
+                          decision_out=dec, score_out=score, workspace=ws_qg)
+
+    def qc():
+        ops.q_change(t["q_tgt"], q_prev, out=d_out, workspace=ws)
+
+    def gate():
+        ops.gate(d_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec, score_out=score)
+
+    ms["qcg_hot"] = timed_hot(qcg)
+    ms["qc"], ms["qc_hot"] = timed(qc), timed_hot(qc)
+    ms["gate"], ms["gate_hot"] = timed(gate), timed_hot(gate)
 
     # Diagnostics sidecar kernels (read-only probes), at the same shapes.
     ws_kv = ops.kv_drift_workspace(t["k_ref"])
@@ -341,10 +376,13 @@ def main():
         "small_kernels": {
             "q_change_gate_us": round(ms["qcg"] * 1e3, 2),
             "q_change_gate_gbs": round((qc_bytes + B * H * n_tgt * 4) / (ms["qcg"] * 1e-3) / 1e9, 1),
+            "q_change_gate_hot_us": round(ms["qcg_hot"] * 1e3, 2),
             "q_change_us": round(ms["qc"] * 1e3, 2),
             "q_change_gbs": round(qc_bytes / (ms["qc"] * 1e-3) / 1e9, 1),
+            "q_change_hot_us": round(ms["qc_hot"] * 1e3, 2),
             "gate_us": round(ms["gate"] * 1e3, 2),
             "gate_gbs": round((B * H * n_tgt * 4 + B * H * 4) / (ms["gate"] * 1e-3) / 1e9, 1),
+            "gate_hot_us": round(ms["gate_hot"] * 1e3, 2),
             "commit_us": round(ms["commit"] * 1e3, 2),
             "diag_kv_drift_us": round(ms["kv_drift"] * 1e3, 2),
             "diag_kv_drift_gbs": round(diag_bytes["kv_drift"] / (ms["kv_drift"] * 1e-3) / 1e9, 1),

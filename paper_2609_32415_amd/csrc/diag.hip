@@ -32,6 +32,7 @@ namespace refadapt {
 namespace {
 
 constexpr int MM_THREADS = 256;
+constexpr int MM_UNROLL = 8;
 constexpr int AC_THREADS = 64;
 
 // Pass 1: workgroup (chunk, bh, pair) sums (cur - base)^2 and base^2 over its rows.
@@ -82,7 +83,16 @@ __global__ __launch_bounds__(MM_THREADS) void mass_mean_kernel(const float* mass
   const int bh = blockIdx.x;
   const float* m = mass + (int64_t)bh * n;
   float s = 0.f;
-  for (int i = threadIdx.x; i < n; i += MM_THREADS) s += complement ? 1.f - m[i] : m[i];
+  // MM_UNROLL loads per thread in flight; the additions keep the plain strided order.
+  for (int i0 = threadIdx.x; i0 < n; i0 += MM_UNROLL * MM_THREADS) {
+    float v[MM_UNROLL];
+#pragma unroll
+    for (int u = 0; u < MM_UNROLL; ++u) v[u] = i0 + u * MM_THREADS < n ? m[i0 + u * MM_THREADS] : 0.f;
+#pragma unroll
+    for (int u = 0; u < MM_UNROLL; ++u) {
+      if (i0 + u * MM_THREADS < n) s += complement ? 1.f - v[u] : v[u];
+    }
+  }
   s = wave_sum(s);
   __shared__ float red[MM_THREADS / 64];
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;

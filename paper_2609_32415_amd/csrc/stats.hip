@@ -48,13 +48,30 @@ __global__ __launch_bounds__(256) void q_change_final(const float2* ws, int32_t 
 // computes), then COMPUTE if an earlier block reactivated, else REACTIVATE when the
 // head-mean score reaches theta, else REUSE. d[i], m[i] are the Q-change and the mean
 // lagged mass of (b, h) pair i; the head means are taken in fp64 in index order.
+// The state and this block's thresholds come in registers (the kernels load them before
+// their reductions, so the loads' latency is hidden); the updated state is stored back.
+struct GateInputs {
+  GateState st;
+  float th0, th1;  // theta[block], or theta[2 block], theta[2 block + 1] for the AND mode
+};
+
+__device__ __forceinline__ GateInputs gate_load(const GateState* st, const float* theta, int32_t block,
+                                                int32_t mode) {
+  GateInputs g;
+  g.st = *st;
+  g.th0 = theta[mode == 3 ? 2 * block : block];
+  g.th1 = mode == 3 ? theta[2 * block + 1] : 0.f;
+  return g;
+}
+
 __device__ void gate_decide(int32_t BH, int32_t block, int32_t step, int32_t mode, const float* d, const float* m,
-                            const float* theta, GateState* st, int32_t* decision_out, float* score_out) {
+                            GateInputs g, GateState* st, int32_t* decision_out, float* score_out) {
+  GateState s = g.st;
   if (block == 0) {
-    const bool full = step == 0 || (st->delta_max > 0 && step - st->a_full >= st->delta_max);
-    if (full) st->a_full = step;
-    st->reactivated = full ? 1 : 0;
-    st->step = step;
+    const bool full = step == 0 || (s.delta_max > 0 && step - s.a_full >= s.delta_max);
+    if (full) s.a_full = step;
+    s.reactivated = full ? 1 : 0;
+    s.step = step;
   }
   double sd = 0.0, sm = 0.0, sg = 0.0;
   for (int i = 0; i < BH; ++i) {
@@ -65,22 +82,23 @@ __device__ void gate_decide(int32_t BH, int32_t block, int32_t step, int32_t mod
   }
   const double dm = sd / BH, mm = sm / BH, gm = sg / BH;
   int dec;
-  if (st->reactivated) {
+  if (s.reactivated) {
     dec = DEC_COMPUTE;
   } else {
     bool cross;
     if (mode == 0) {
-      cross = gm >= (double)theta[block];
+      cross = gm >= (double)g.th0;
     } else if (mode == 1) {
-      cross = dm >= (double)theta[block];
+      cross = dm >= (double)g.th0;
     } else if (mode == 2) {
-      cross = mm >= (double)theta[block];
+      cross = mm >= (double)g.th0;
     } else {
-      cross = dm >= (double)theta[2 * block] && mm >= (double)theta[2 * block + 1];
+      cross = dm >= (double)g.th0 && mm >= (double)g.th1;
     }
     dec = cross ? DEC_REACTIVATE : DEC_REUSE;
-    if (cross) st->reactivated = 1;
+    if (cross) s.reactivated = 1;
   }
+  *st = s;
   *decision_out = dec;
   score_out[0] = (float)dm;
   score_out[1] = (float)mm;
@@ -88,16 +106,22 @@ __device__ void gate_decide(int32_t BH, int32_t block, int32_t step, int32_t mod
 }
 
 constexpr int GATE_THREADS = 1024;
+constexpr int GATE_UNROLL = 16;  // 16-byte loads per lane in flight
 
 __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t n_tgt, int32_t block, int32_t step,
                                                             int32_t mode, const float* d_cur, const float* mass_prev,
                                                             const float* theta, GateState* st, int32_t* decision_out,
                                                             float* score_out) {
-  extern __shared__ float m_head[];  // [BH] mean lagged mass per (b, h)
+  extern __shared__ float s_dm[];  // [2 * BH]: D (copied from d_cur), then the mean lagged mass
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  GateInputs gin;
+  if (tid == 0) gin = gate_load(st, theta, block, mode);
+  for (int i = tid; i < BH; i += GATE_THREADS) s_dm[i] = d_cur[i];
 
   // Mean over target queries of the lagged per-query reference mass, one wavefront per
-  // (b, h): 16-byte loads, four in flight per lane, then a fixed-order butterfly.
+  // (b, h): 16-byte loads, GATE_UNROLL in flight per lane (a 4096-query row is one round
+  // trip to memory), then a fixed-order butterfly. Loads past the row's end read as zeros,
+  // which add exactly +0.
   for (int bh = wave; bh < BH; bh += GATE_THREADS / 64) {
     const float* row = mass_prev + (int64_t)bh * n_tgt;
     float s = 0.f;
@@ -106,30 +130,30 @@ __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t 
       const int n4 = n_tgt >> 2;
       const float4* r4 = reinterpret_cast<const float4*>(row);
       float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-      int k = lane;
-      for (; k + 192 < n4; k += 256) {
-        const float4 a = r4[k], b2 = r4[k + 64], c2 = r4[k + 128], d2 = r4[k + 192];
-        acc.x += (a.x + b2.x) + (c2.x + d2.x);
-        acc.y += (a.y + b2.y) + (c2.y + d2.y);
-        acc.z += (a.z + b2.z) + (c2.z + d2.z);
-        acc.w += (a.w + b2.w) + (c2.w + d2.w);
-      }
-      for (; k < n4; k += 64) {
-        const float4 a = r4[k];
-        acc.x += a.x;
-        acc.y += a.y;
-        acc.z += a.z;
-        acc.w += a.w;
+      for (int k0 = lane; k0 < n4; k0 += 64 * GATE_UNROLL) {
+        float4 v[GATE_UNROLL];
+#pragma unroll
+        for (int u = 0; u < GATE_UNROLL; ++u) {
+          const int k = k0 + 64 * u;
+          v[u] = k < n4 ? r4[k] : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < GATE_UNROLL; ++u) {
+          acc.x += v[u].x;
+          acc.y += v[u].y;
+          acc.z += v[u].z;
+          acc.w += v[u].w;
+        }
       }
       s = (acc.x + acc.y) + (acc.z + acc.w);
       i0 = n4 << 2;
     }
     for (int i = i0 + lane; i < n_tgt; i += 64) s += row[i];
     s = wave_sum(s);
-    if (lane == 0) m_head[bh] = s / (float)n_tgt;
+    if (lane == 0) s_dm[BH + bh] = s / (float)n_tgt;
   }
   __syncthreads();
-  if (tid == 0) gate_decide(BH, block, step, mode, d_cur, m_head, theta, st, decision_out, score_out);
+  if (tid == 0) gate_decide(BH, block, step, mode, s_dm, s_dm + BH, gin, st, decision_out, score_out);
 }
 
 // Q-change and gate in two launches (instead of three). Pass 1: workgroup (chunk, bh)
@@ -167,6 +191,8 @@ __global__ __launch_bounds__(QG_THREADS) void q_change_gate_final(const float4* 
                                                                   GateState* st, float* d_out, int32_t* decision_out,
                                                                   float* score_out) {
   extern __shared__ float s_dm[];  // [2 * BH]: D, then the mean lagged mass of each (b, h)
+  GateInputs gin;
+  if (threadIdx.x == 0) gin = gate_load(st, theta, block, mode);
   for (int i = threadIdx.x; i < BH; i += QG_THREADS) {
     double a = 0.0, c = 0.0, ms = 0.0;
     for (int k = 0; k < chunks; ++k) {
@@ -181,7 +207,7 @@ __global__ __launch_bounds__(QG_THREADS) void q_change_gate_final(const float4* 
     s_dm[BH + i] = (float)(ms / n_rows);
   }
   __syncthreads();
-  if (threadIdx.x == 0) gate_decide(BH, block, step, mode, s_dm, s_dm + BH, theta, st, decision_out, score_out);
+  if (threadIdx.x == 0) gate_decide(BH, block, step, mode, s_dm, s_dm + BH, gin, st, decision_out, score_out);
 }
 
 constexpr int CC_THREADS = 256;
@@ -242,8 +268,8 @@ hipError_t launch_gate(int32_t B, int32_t H, int32_t n_tgt, int32_t block, int32
                        const float* d_cur, const float* mass_prev, const float* theta, GateState* state,
                        int32_t* decision_out, float* score_out, hipStream_t stream) {
   const int bh = B * H;
-  return launch_kernel(gate_kernel, dim3(1), dim3(GATE_THREADS), bh * sizeof(float), stream, bh, n_tgt, block, step,
-                       mode, d_cur, mass_prev, theta, state, decision_out, score_out);
+  return launch_kernel(gate_kernel, dim3(1), dim3(GATE_THREADS), 2 * (size_t)bh * sizeof(float), stream, bh, n_tgt,
+                       block, step, mode, d_cur, mass_prev, theta, state, decision_out, score_out);
 }
 
 size_t q_change_gate_workspace_bytes(int32_t B, int32_t H, int32_t n_tgt, int32_t head_dim) {
