@@ -654,7 +654,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 // A chunk's reference max never exceeds its running max, so M bounds both;
 // summing the reference part against M_R keeps lse_ref finite when the target
 // keys score so far above the reference keys that 2^(M_R - M) underflows.
-template <int D>
+template <int D, int MERGE_BATCH>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   constexpr int TPR = D / 4, RPB = 256 / TPR;
   bool tgt_only = false;
@@ -674,26 +674,48 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const int qrow = qt * BM + rr;
   if (qrow >= n_rows) return;
 
-  const int64_t base = (int64_t)st * pl.chunks * BM + rr;  // partial row of chunk 0
+  // Both passes load MERGE_BATCH chunks' partials before using any (one memory round trip
+  // per batch instead of per chunk) and combine them in chunk order.
+  const int nc = pl.chunks;
+  const int64_t base = (int64_t)st * nc * BM + rr;  // partial row of chunk 0
   float M = -__builtin_inff(), M_R = -__builtin_inff();
-  for (int c = 0; c < pl.chunks; ++c) {
-    const float4 sv = p.part_st[base + (int64_t)c * BM];
-    M = fmaxf(M, sv.x);
-    if (sv.w > 0.f) M_R = fmaxf(M_R, sv.z);
+  for (int c0 = 0; c0 < nc; c0 += MERGE_BATCH) {
+    float4 sv[MERGE_BATCH];
+#pragma unroll
+    for (int u = 0; u < MERGE_BATCH; ++u)
+      if (c0 + u < nc) sv[u] = p.part_st[base + (int64_t)(c0 + u) * BM];
+#pragma unroll
+    for (int u = 0; u < MERGE_BATCH; ++u) {
+      if (c0 + u < nc) {
+        M = fmaxf(M, sv[u].x);
+        if (sv[u].w > 0.f) M_R = fmaxf(M_R, sv[u].z);
+      }
+    }
   }
   float L_Rr = 0.f, L_Y = 0.f;  // L_Rr: reference sum against M_R
   float4 acc{0.f, 0.f, 0.f, 0.f};
-  for (int c = 0; c < pl.chunks; ++c) {
-    const int64_t prow = base + (int64_t)c * BM;
-    const float4 sv = p.part_st[prow];
-    const float wgt = __builtin_amdgcn_exp2f(sv.x - M);
-    L_Y += sv.y * wgt;
-    if (sv.w > 0.f) L_Rr += sv.w * __builtin_amdgcn_exp2f(sv.z - M_R);
-    const float4 ov = *reinterpret_cast<const float4*>(p.part_o + prow * D + col);
-    acc.x += ov.x * wgt;
-    acc.y += ov.y * wgt;
-    acc.z += ov.z * wgt;
-    acc.w += ov.w * wgt;
+  for (int c0 = 0; c0 < nc; c0 += MERGE_BATCH) {
+    float4 sv[MERGE_BATCH], ov[MERGE_BATCH];
+#pragma unroll
+    for (int u = 0; u < MERGE_BATCH; ++u) {
+      if (c0 + u < nc) {
+        const int64_t prow = base + (int64_t)(c0 + u) * BM;
+        sv[u] = p.part_st[prow];
+        ov[u] = *reinterpret_cast<const float4*>(p.part_o + prow * D + col);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < MERGE_BATCH; ++u) {
+      if (c0 + u < nc) {
+        const float wgt = __builtin_amdgcn_exp2f(sv[u].x - M);
+        L_Y += sv[u].y * wgt;
+        if (sv[u].w > 0.f) L_Rr += sv[u].w * __builtin_amdgcn_exp2f(sv[u].z - M_R);
+        acc.x += ov[u].x * wgt;
+        acc.y += ov[u].y * wgt;
+        acc.z += ov[u].z * wgt;
+        acc.w += ov[u].w * wgt;
+      }
+    }
   }
   const float L_R = L_Rr > 0.f ? L_Rr * __builtin_amdgcn_exp2f(M_R - M) : 0.f;
   const float total = L_R + L_Y;
@@ -766,8 +788,13 @@ hipError_t launch_attn_bf16(const AttnParams& p, int head_dim, hipStream_t strea
   if (split == 0) return hipSuccess;
   const int rpb = 256 / (head_dim / 4);
   const dim3 mgrid((split * BM + rpb - 1) / rpb);
-  return head_dim == 128 ? launch_kernel(attn_merge_kernel<128>, mgrid, dim3(256), 0, stream, p)
-                         : launch_kernel(attn_merge_kernel<64>, mgrid, dim3(256), 0, stream, p);
+  // Loads in flight per merge thread: all chunks of a two-chunk split, else eight at a time.
+  const bool two = max(p.plan[0].chunks, p.plan[1].chunks) <= 2;
+  if (head_dim == 128)
+    return two ? launch_kernel(attn_merge_kernel<128, 2>, mgrid, dim3(256), 0, stream, p)
+               : launch_kernel(attn_merge_kernel<128, 8>, mgrid, dim3(256), 0, stream, p);
+  return two ? launch_kernel(attn_merge_kernel<64, 2>, mgrid, dim3(256), 0, stream, p)
+             : launch_kernel(attn_merge_kernel<64, 8>, mgrid, dim3(256), 0, stream, p);
 }
 
 }  // namespace refadapt
