@@ -322,6 +322,8 @@ def main():
     ms["qcg_hot"] = timed_hot(qcg)
     ms["qc"], ms["qc_hot"] = timed(qc), timed_hot(qc)
     ms["gate"], ms["gate_hot"] = timed(gate), timed_hot(gate)
+    # The cache commit of a computed block: copies the fresh reference K/V into the cache.
+    ms["commit_copy"] = timed(lambda: ops.cache_commit(t["k_ref"], t["v_ref"], commit_k, commit_v))
 
     # Diagnostics sidecar kernels (read-only probes), at the same shapes.
     ws_kv = ops.kv_drift_workspace(t["k_ref"])
@@ -384,6 +386,8 @@ def main():
             "gate_gbs": round((B * H * n_tgt * 4 + B * H * 4) / (ms["gate"] * 1e-3) / 1e9, 1),
             "gate_hot_us": round(ms["gate_hot"] * 1e3, 2),
             "commit_us": round(ms["commit"] * 1e3, 2),
+            "commit_copy_us": round(ms["commit_copy"] * 1e3, 2),
+            "commit_copy_gbs": round(4 * B * H * n_ref * D * 2 / (ms["commit_copy"] * 1e-3) / 1e9, 1),
             "diag_kv_drift_us": round(ms["kv_drift"] * 1e3, 2),
             "diag_kv_drift_gbs": round(diag_bytes["kv_drift"] / (ms["kv_drift"] * 1e-3) / 1e9, 1),
             "diag_drift_log_ratio_us": round(ms["ratio"] * 1e3, 2),
