@@ -113,6 +113,41 @@ def test_gate_sequence_matches_oracle(mode):
         assert st[1] == a_full and st[3] == t
 
 
+@pytest.mark.parametrize("B,H", [(1, 8192), (2, 4096)])
+def test_gate_at_the_batch_heads_limit(B, H):
+    """batch * heads = 8192, the largest the gate entry points take (their per-head
+    D and mean-mass tables then fill 64 KiB of LDS): refadapt_gate and the fused
+    refadapt_q_change_gate reproduce the oracle's D, scores and decision."""
+    print(f"gate limit {B}x{H}", flush=True)
+    n, d_head = 5, 64
+    rng = np.random.default_rng(11)
+    q0 = rng.standard_normal((B, H, n, d_head)).astype(np.float32)
+    q1 = (q0 + 0.3 * rng.standard_normal(q0.shape)).astype(np.float32)
+    m = rng.uniform(0.0, 1.0, (B, H, n)).astype(np.float32)
+    d_ref = q_change(q1, q0, 1e-8)
+    theta_v = 0.15
+    theta = torch.full((1,), theta_v, dtype=torch.float32, device="cuda:0")
+    exp = gate(d_ref.astype(np.float32), m, theta_v, False)
+    # The separate gate on the oracle's D.
+    state = ops.new_gate_state("cuda:0")
+    ops.gate(dev(d_ref.astype(np.float32), "f32"), dev(m, "f32"), theta, state, 0, 0, "product")  # step 0
+    dec, score = ops.gate(dev(d_ref.astype(np.float32), "f32"), dev(m, "f32"), theta, state, 0, 1, "product")
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(host(score), [exp.d_mean, exp.m_mean, exp.g_mean], rtol=1e-5, atol=1e-7)
+    if abs(exp.g_mean - theta_v) > 1e-4:
+        assert int(dec.item()) == exp.decision
+    # The fused path computes D itself.
+    state = ops.new_gate_state("cuda:0")
+    ops.gate(dev(d_ref.astype(np.float32), "f32"), dev(m, "f32"), theta, state, 0, 0, "product")  # step 0
+    d_got, dec, score = ops.q_change_gate(dev(q1, "f32"), dev(q0, "f32"), dev(m, "f32"), theta, state, 0, 1,
+                                          "product", eps=1e-8)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(host(d_got), d_ref, rtol=1e-5, atol=0)
+    np.testing.assert_allclose(host(score), [exp.d_mean, exp.m_mean, exp.g_mean], rtol=1e-5, atol=1e-7)
+    if abs(exp.g_mean - theta_v) > 1e-4:
+        assert int(dec.item()) == exp.decision
+
+
 @pytest.mark.parametrize("mode", ["product", "and"])
 @pytest.mark.parametrize("dtype,B,H,n,d", [("bf16", 1, 24, 4096, 128), ("bf16", 2, 3, 333, 64), ("f32", 1, 2, 100, 64)])
 def test_fused_q_change_gate_matches_oracle(mode, dtype, B, H, n, d):
