@@ -113,6 +113,12 @@ typedef struct {
   int32_t seg_end[RA_MAX_SEG];   /* increasing; multiples of 64 except seg_end[n_seg-1] == n_ref */
   uint32_t seg_cache;            /* RA_KV_SEGMENTS: bit s selects the cached K/V for segment s */
   float* seg_mass;               /* out [B, H, n_tgt, n_seg] target-query mass per segment, or NULL */
+  /* Cached reference queries [B, H, n_ref, d] (the queries of the block's cached reference
+   * state), or NULL data. When given, reference queries that attend over the cached
+   * reference K/V read them instead of q_ref: under RA_KV_CACHE with RA_Q_ALL, and on
+   * REACTIVATE under RA_KV_DEVICE (Alg. 1 boundary branch: the cached reference state is
+   * restored and its queries attend to [cached K_R; current K_Y]). */
+  ra_tensor q_cache;
 } ra_attn_args;
 
 /*
@@ -164,7 +170,8 @@ typedef struct {
  * or a required pointer that is NULL (q/k/v/o_tgt always; k_ref/v_ref when
  * fresh K/V may be read and n_ref > 0; k_cache/v_cache when cached K/V may be
  * read and n_ref > 0; q_ref/o_ref when reference queries may attend and
- * n_ref > 0; decision under RA_KV_DEVICE; n_seg outside 1..RA_MAX_SEG or
+ * n_ref > 0, except q_ref under RA_KV_CACHE when q_cache is given; decision
+ * under RA_KV_DEVICE; n_seg outside 1..RA_MAX_SEG or
  * segment ends that do not increase to n_ref). RA_EUNSUPPORTED for head_dim not
  * in {64, 128} or misaligned tensors or workspace, and for segments with
  * RA_F32, RA_KV_DEVICE, an inner boundary off the 64-row key tiles, or (under
@@ -259,19 +266,24 @@ ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, in
                                  size_t ws_bytes, void* stream);
 
 /*
- * refadapt_cache_commit - refresh a block's reference K/V cache.
+ * refadapt_cache_commit - refresh a block's cached reference state.
  *
- * Copies k_ref -> k_cache and v_ref -> v_cache ([B, H, n_ref, d]) when
- * `decision` is NULL or *decision == RA_COMPUTE, and then writes `step` to
- * *age when age is non-NULL (Alg. 1: a computing block updates its cached
- * K/V and sets its materialisation step a_b). Otherwise nothing is written.
- * With v_ref and v_cache both of NULL data only k_ref -> k_cache is copied
- * (e.g. the target Q kept as the block's materialisation anchor).
- * Errors: RA_EINVAL (null tensors, sizes), RA_EUNSUPPORTED (alignment).
+ * Copies k_ref -> k_cache, v_ref -> v_cache and q_ref -> q_cache
+ * ([B, H, n_ref, d]) when `decision` is NULL or *decision == RA_COMPUTE, and
+ * then writes `step` to *age when age is non-NULL (Alg. 1: a computing block
+ * updates its cached K/V and sets its materialisation step a_b; the cached
+ * queries are those of the same state, read again at a later boundary). Otherwise
+ * nothing is written. K is required; each of the V and Q pairs is copied when
+ * both of its tensors have non-NULL data and skipped when both are NULL (e.g.
+ * K alone for the target Q kept as the block's materialisation anchor). All
+ * pairs are copied by one launch.
+ * Errors: RA_EINVAL (null K tensors, a V or Q pair with one NULL side, sizes),
+ * RA_EUNSUPPORTED (alignment).
  */
 ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int32_t head_dim, int32_t dtype,
-                                ra_tensor k_ref, ra_tensor v_ref, ra_tensor k_cache, ra_tensor v_cache,
-                                const int32_t* decision, int32_t* age, int32_t step, void* stream);
+                                ra_tensor k_ref, ra_tensor v_ref, ra_tensor q_ref, ra_tensor k_cache,
+                                ra_tensor v_cache, ra_tensor q_cache, const int32_t* decision, int32_t* age,
+                                int32_t step, void* stream);
 
 /* ---- Diagnostics sidecar --------------------------------------------------
  *

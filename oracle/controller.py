@@ -7,29 +7,34 @@ per-step Q/K/V tensors are supplied by the caller (``inputs(t, b)``), so the
 loop exercises exactly the parts of Alg. 1 that act on attention:
 
 * step 0 materialises every block (full joint attention on fresh K/V), fills
-  each block's reference K/V cache and records target Q and the realised
-  per-query reference mass;
+  each block's cache with its reference Q/K/V and records target Q and the
+  realised per-query reference mass;
 * a step with ``t - a_full >= delta_max`` recomputes every block from block 0,
   refreshes all caches and sets ``a_full = t`` (bounded-age refresh);
 * otherwise blocks are scanned shallow to deep: before the first crossing a
   block reuses (target queries attend to the cached reference K/V), the first
-  block whose head-mean score reaches theta reactivates (all queries attend,
-  reference K/V still from the cache, cache unchanged), and every deeper
-  block computes on fresh reference K/V and refreshes its cache (age = t);
+  block whose head-mean score reaches theta reactivates (the block's cached
+  reference state is restored: its reference queries and the current target
+  queries attend over the cached reference K/V and the current target K/V;
+  cache unchanged), and every deeper block computes on fresh reference Q/K/V
+  and refreshes its cache (age = t);
 * every block records its target Q and the realised target->reference mass
   of the attention it executed, for the next step.
 
 ``cue="anchor"`` replaces the target-side cue by the change from the block's
-most recent materialisation anchor (App. C, anchor-relative target-Q change):
+most recent materialisation anchor (App. A.2, anchor-relative target-Q change):
 D is measured against the target Q the block had at its last COMPUTE step
 a_b, not at the previous step; the gate is otherwise the same (the paper's
 Anchor-Q x Exposure ablation).
 
 Reading taken where the paper relies on the DiT: at the boundary block the
-paper restores the cached reference hidden state and recomputes the
-reference rows from it; without a DiT, the reference K/V at the boundary are
-the cached ones (which are the K/V of that cached hidden state), so the
-boundary runs all queries over the cache and leaves it unchanged.
+paper restores the cached reference hidden state and runs the reference-query
+computation from it (Alg. 1 boundary branch; Sec. 4 "Execution and cache
+state": the block cache holds that state and its K/V). Without a DiT, the
+cache keeps the state's reference Q, K and V from the block's last COMPUTE
+step, so the boundary's reference rows attend with those cached queries over
+[cached K_R; current K_Y], the target rows with their current queries over
+the same keys, and the cache is left unchanged.
 
 ``local_impact`` is the Sec. 3.3 local-impact equation, used to report the
 executed target output's relative change against the full-fresh output.
@@ -99,6 +104,7 @@ def run_controller(
 
     cache_k = [None] * n_blocks
     cache_v = [None] * n_blocks
+    cache_q = [None] * n_blocks  # reference queries of the cached state
     q_rec = [None] * n_blocks
     q_anchor = [None] * n_blocks  # target Q at the block's last COMPUTE step
     mass_rec = [None] * n_blocks
@@ -112,7 +118,6 @@ def run_controller(
         reactivated = False
         for b in range(n_blocks):
             x = inputs(t, b)
-            q_all = np.concatenate([x["q_ref"], x["q_tgt"]], axis=-2)
             n_ref = x["k_ref"].shape[-2]
             fresh = joint_attention(x["q_tgt"], x["k_ref"], x["v_ref"], x["k_tgt"], x["v_tgt"], scale)
 
@@ -133,14 +138,17 @@ def run_controller(
                     d_mean[t, b], m_mean[t, b], g_mean[t, b] = res.d_mean, res.m_mean, res.g_mean
 
             if dec == COMPUTE:
+                q_all = np.concatenate([x["q_ref"], x["q_tgt"]], axis=-2)
                 ex = joint_attention(q_all, x["k_ref"], x["v_ref"], x["k_tgt"], x["v_tgt"], scale)
                 o_tgt = ex["o"][..., n_ref:, :]
                 mass_tgt = ex["ref_mass"][..., n_ref:]
                 cache_k[b] = np.array(x["k_ref"], dtype=np.float64)
                 cache_v[b] = np.array(x["v_ref"], dtype=np.float64)
+                cache_q[b] = np.array(x["q_ref"], dtype=np.float64)
                 q_anchor[b] = np.array(x["q_tgt"], dtype=np.float64)
                 age[b] = t
-            elif dec == REACTIVATE:
+            elif dec == REACTIVATE:  # restored state: its reference queries, current target queries
+                q_all = np.concatenate([cache_q[b], x["q_tgt"]], axis=-2)
                 ex = joint_attention(q_all, cache_k[b], cache_v[b], x["k_tgt"], x["v_tgt"], scale)
                 o_tgt = ex["o"][..., n_ref:, :]
                 mass_tgt = ex["ref_mass"][..., n_ref:]

@@ -100,6 +100,7 @@ class ra_attn_args(ctypes.Structure):
         ("seg_end", ctypes.c_int32 * RA_MAX_SEG),
         ("seg_cache", ctypes.c_uint32),
         ("seg_mass", ctypes.c_void_p),
+        ("q_cache", ra_tensor),
     ]
 
 
@@ -141,7 +142,8 @@ def _load():
     lib.refadapt_q_change_gate.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, i32, i32, i32,
                                            vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.refadapt_q_change_gate.restype = i32
-    lib.refadapt_cache_commit.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor, ra_tensor, vp, vp, i32, vp]
+    lib.refadapt_cache_commit.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor, ra_tensor,
+                                          ra_tensor, ra_tensor, vp, vp, i32, vp]
     lib.refadapt_cache_commit.restype = i32
     lib.refadapt_kv_drift_workspace_size.argtypes = [i32, i32, i32, i32]
     lib.refadapt_kv_drift_workspace_size.restype = ctypes.c_size_t
@@ -210,8 +212,10 @@ def refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, 
                                              workspace, ws_bytes, stream))
 
 
-def refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, k_cache, v_cache, decision, age, step, stream):
-    return _check(LIB.refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, k_cache, v_cache, decision, age, step, stream))
+def refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, q_ref, k_cache, v_cache, q_cache,
+                          decision, age, step, stream):
+    return _check(LIB.refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, q_ref, k_cache,
+                                            v_cache, q_cache, decision, age, step, stream))
 
 
 def refadapt_kv_drift_workspace_size(batch, heads, n_rows, head_dim):

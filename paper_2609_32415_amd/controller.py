@@ -9,9 +9,11 @@ without any host synchronisation:
                        the bounded-age refresh make every block of the step compute);
                        two launches (fused=False: refadapt_q_change + refadapt_gate, three)
   refadapt_joint_attn  RA_KV_DEVICE: REUSE -> target queries over the cached
-                       reference K/V; REACTIVATE -> all queries over the cache;
+                       reference K/V; REACTIVATE -> current target queries and the
+                       cached reference queries over the cache (the boundary
+                       restores the block's cached reference state);
                        COMPUTE -> all queries over fresh K/V
-  refadapt_cache_commit  fresh reference K/V -> cache and a_b <- t on COMPUTE
+  refadapt_cache_commit  fresh reference K/V and Q -> cache and a_b <- t on COMPUTE
 
 and records the block's target Q (by reference) and the per-query reference
 mass of the attention it executed (ping-pong buffers) for the next step. The
@@ -59,6 +61,9 @@ class Controller:
         self.state = ops.new_gate_state(device, delta_max or 0)
         self.k_cache = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
         self.v_cache = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
+        # reference queries of each block's cached state: the boundary restores that state, so
+        # its reference rows attend with them (Alg. 1 boundary branch)
+        self.q_cache = [torch.empty(self.shape_r, dtype=dtype, device=device) for _ in range(n_blocks)]
         self.mass = [[torch.zeros((batch, heads, n_tgt), dtype=torch.float32, device=device) for _ in range(2)]
                      for _ in range(n_blocks)]
         self.parity = [0] * n_blocks
@@ -99,13 +104,13 @@ class Controller:
         nxt = 1 - self.parity[b]
         ops.joint_attn(
             x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"], v_ref=x["v_ref"],
-            k_cache=self.k_cache[b], v_cache=self.v_cache[b], kvsrc="device", decision=dec,
+            k_cache=self.k_cache[b], v_cache=self.v_cache[b], q_cache=self.q_cache[b], kvsrc="device", decision=dec,
             o_tgt=self.o_tgt[b], o_ref=self.o_ref[b], ref_mass=self.mass[b][nxt], workspace=self.attn_ws,
         )
         if self.sidecar is not None:  # read-only probes; the block's cache still holds its anchor K/V
             self.sidecar.block(t, b, x, self)
         ops.cache_commit(x["k_ref"], x["v_ref"], self.k_cache[b], self.v_cache[b], decision=dec,
-                         age=self.age[b:b + 1], step=t)
+                         age=self.age[b:b + 1], step=t, q_ref=x["q_ref"], q_cache=self.q_cache[b])
         if self.cue == "anchor":
             ops.cache_commit(x["q_tgt"], None, self.q_anchor[b], None, decision=dec)
         self.q_prev[b] = x["q_tgt"]

@@ -219,8 +219,12 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
     if ((s = check_tensor("k_cache", a.k_cache, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
     if ((s = check_tensor("v_cache", a.v_cache, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
   }
+  // Cached reference queries: read where reference queries attend over the cached K/V.
+  const bool q_cache = ref_queries && a.q_cache.data != nullptr && (d.kvsrc == RA_KV_CACHE || device);
   if (ref_queries) {
-    if ((s = check_tensor("q_ref", a.q_ref, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
+    if (!(q_cache && d.kvsrc == RA_KV_CACHE))
+      if ((s = check_tensor("q_ref", a.q_ref, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
+    if (q_cache && (s = check_tensor("q_cache", a.q_cache, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
     if ((s = check_tensor("o_ref", a.o_ref, d.dtype, d.n_ref, d.head_dim)) != RA_OK) return s;
   }
   if (device && a.decision == nullptr) return fail(RA_EINVAL, "joint_attn: RA_KV_DEVICE needs a decision pointer");
@@ -247,6 +251,7 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   p.k_tgt = view(a.k_tgt);
   p.v_tgt = view(a.v_tgt);
   p.q_ref = view(a.q_ref);
+  p.q_cache = q_cache ? view(a.q_cache) : View{nullptr, 0, 0, 0};
   p.k_fresh = view(a.k_ref);
   p.v_fresh = view(a.v_ref);
   p.k_cache = view(a.k_cache);
@@ -355,26 +360,46 @@ size_t refadapt_q_change_gate_workspace_size(int32_t batch, int32_t heads, int32
   return q_change_gate_workspace_bytes(batch, heads, n_tgt, head_dim);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Arguments of the fused Q-change + gate other than its workspace (`who` names the caller).
+ra_status check_q_change_gate(const char* who, int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim,
+                              int32_t dtype, const ra_tensor& q_cur, const ra_tensor& q_prev, float eps,
+                              int32_t block, int32_t step, int32_t mode, const float* mass_prev, const float* theta,
+                              const ra_gate_state* state, const float* d_out, const int32_t* decision_out,
+                              const float* score_out) {
+  if (batch < 1 || heads < 1 || n_tgt < 1) return fail(RA_EINVAL, "%s: batch, heads, n_tgt must be >= 1", who);
+  if ((int64_t)batch * heads > 8192) return fail(RA_EUNSUPPORTED, "%s: batch*heads must be <= 8192", who);
+  if (dtype != RA_BF16 && dtype != RA_F32) return fail(RA_EINVAL, "%s: unknown dtype %d", who, dtype);
+  if (head_dim < 1 || head_dim % (dtype == RA_BF16 ? 8 : 4) != 0)
+    return fail(RA_EUNSUPPORTED, "%s: head_dim %d must be a positive multiple of %d", who, head_dim,
+                dtype == RA_BF16 ? 8 : 4);
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RA_EINVAL, "%s: eps must be finite and >= 0", who);
+  if (block < 0 || step < 0) return fail(RA_EINVAL, "%s: block and step must be >= 0", who);
+  if (mode < RA_GATE_PRODUCT || mode > RA_GATE_AND) return fail(RA_EINVAL, "%s: unknown mode %d", who, mode);
+  ra_status s;
+  if ((s = check_tensor("q_cur", q_cur, dtype, n_tgt, head_dim)) != RA_OK) return s;
+  if ((s = check_tensor("q_prev", q_prev, dtype, n_tgt, head_dim)) != RA_OK) return s;
+  if (!mass_prev || !theta || !state || !d_out || !decision_out || !score_out)
+    return fail(RA_EINVAL, "%s: null pointer argument", who);
+  return RA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim, int32_t dtype,
                                  ra_tensor q_cur, ra_tensor q_prev, float eps, int32_t block, int32_t step,
                                  int32_t mode, const float* mass_prev, const float* theta, ra_gate_state* state,
                                  float* d_out, int32_t* decision_out, float* score_out, void* workspace,
                                  size_t ws_bytes, void* stream) {
-  if (batch < 1 || heads < 1 || n_tgt < 1)
-    return fail(RA_EINVAL, "q_change_gate: batch, heads, n_tgt must be >= 1");
-  if ((int64_t)batch * heads > 8192) return fail(RA_EUNSUPPORTED, "q_change_gate: batch*heads must be <= 8192");
-  if (dtype != RA_BF16 && dtype != RA_F32) return fail(RA_EINVAL, "q_change_gate: unknown dtype %d", dtype);
-  if (head_dim < 1 || head_dim % (dtype == RA_BF16 ? 8 : 4) != 0)
-    return fail(RA_EUNSUPPORTED, "q_change_gate: head_dim %d must be a positive multiple of %d", head_dim,
-                dtype == RA_BF16 ? 8 : 4);
-  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(RA_EINVAL, "q_change_gate: eps must be finite and >= 0");
-  if (block < 0 || step < 0) return fail(RA_EINVAL, "q_change_gate: block and step must be >= 0");
-  if (mode < RA_GATE_PRODUCT || mode > RA_GATE_AND) return fail(RA_EINVAL, "q_change_gate: unknown mode %d", mode);
   ra_status s;
-  if ((s = check_tensor("q_cur", q_cur, dtype, n_tgt, head_dim)) != RA_OK) return s;
-  if ((s = check_tensor("q_prev", q_prev, dtype, n_tgt, head_dim)) != RA_OK) return s;
-  if (!mass_prev || !theta || !state || !d_out || !decision_out || !score_out)
-    return fail(RA_EINVAL, "q_change_gate: null pointer argument");
+  if ((s = check_q_change_gate("q_change_gate", batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block,
+                               step, mode, mass_prev, theta, state, d_out, decision_out, score_out)) != RA_OK)
+    return s;
   const size_t need = refadapt_q_change_gate_workspace_size(batch, heads, n_tgt, head_dim);
   if (workspace == nullptr || ws_bytes < need)
     return fail(RA_EWORKSPACE, "q_change_gate: workspace needs %zu bytes (got %zu)", need, workspace ? ws_bytes : 0);
@@ -388,23 +413,30 @@ ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, in
 }
 
 ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int32_t head_dim, int32_t dtype,
-                                ra_tensor k_ref, ra_tensor v_ref, ra_tensor k_cache, ra_tensor v_cache,
-                                const int32_t* decision, int32_t* age, int32_t step, void* stream) {
+                                ra_tensor k_ref, ra_tensor v_ref, ra_tensor q_ref, ra_tensor k_cache,
+                                ra_tensor v_cache, ra_tensor q_cache, const int32_t* decision, int32_t* age,
+                                int32_t step, void* stream) {
   if (batch < 1 || heads < 1 || n_ref < 0) return fail(RA_EINVAL, "cache_commit: bad sizes");
   if (dtype != RA_BF16 && dtype != RA_F32) return fail(RA_EINVAL, "cache_commit: unknown dtype %d", dtype);
   if (head_dim < 1 || (head_dim * (dtype == RA_BF16 ? 2 : 4)) % 16 != 0)
     return fail(RA_EUNSUPPORTED, "cache_commit: head_dim %d must fill whole 16-byte units", head_dim);
   if (n_ref == 0) return ok();
   ra_status s;
-  if ((s = check_tensor("k_ref", k_ref, dtype, n_ref, head_dim)) != RA_OK) return s;
-  if ((s = check_tensor("k_cache", k_cache, dtype, n_ref, head_dim)) != RA_OK) return s;
-  const bool k_only = v_ref.data == nullptr && v_cache.data == nullptr;
-  if (!k_only) {
-    if ((s = check_tensor("v_ref", v_ref, dtype, n_ref, head_dim)) != RA_OK) return s;
-    if ((s = check_tensor("v_cache", v_cache, dtype, n_ref, head_dim)) != RA_OK) return s;
+  CommitSet cs{};
+  const ra_tensor* src[3] = {&k_ref, &v_ref, &q_ref};
+  const ra_tensor* dst[3] = {&k_cache, &v_cache, &q_cache};
+  const char* src_name[3] = {"k_ref", "v_ref", "q_ref"};
+  const char* dst_name[3] = {"k_cache", "v_cache", "q_cache"};
+  for (int i = 0; i < 3; ++i) {
+    // K is required; V and Q are optional pairs (both sides given, or neither).
+    if (i > 0 && src[i]->data == nullptr && dst[i]->data == nullptr) continue;
+    if ((s = check_tensor(src_name[i], *src[i], dtype, n_ref, head_dim)) != RA_OK) return s;
+    if ((s = check_tensor(dst_name[i], *dst[i], dtype, n_ref, head_dim)) != RA_OK) return s;
+    cs.src[cs.n] = view(*src[i]);
+    cs.dst[cs.n] = view(*dst[i]);
+    ++cs.n;
   }
-  const hipError_t e = launch_cache_commit(dtype, batch, heads, n_ref, head_dim, view(k_ref), view(v_ref),
-                                           view(k_cache), view(v_cache), decision, age, step,
+  const hipError_t e = launch_cache_commit(dtype, batch, heads, n_ref, head_dim, cs, decision, age, step,
                                            static_cast<hipStream_t>(stream));
   return launch_status(e, "cache_commit");
 }

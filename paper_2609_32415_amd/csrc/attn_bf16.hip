@@ -258,7 +258,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const bool ref_rows = qt < qt_ref;
   if (!ref_rows) qt -= qt_ref;
 
-  const View qv = ref_rows ? p.q_ref : p.q_tgt;
+  // Reference queries over the cached K/V read the cached queries when the caller gave them.
+  const View qv = ref_rows ? (use_cache && p.q_cache.p ? p.q_cache : p.q_ref) : p.q_tgt;
   const View ov = ref_rows ? p.o_ref : p.o_tgt;
   const int n_rows = ref_rows ? p.n_ref : p.n_tgt;
   const View krv = use_cache ? p.k_cache : p.k_fresh;

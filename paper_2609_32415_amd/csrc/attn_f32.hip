@@ -38,7 +38,7 @@ __global__ __launch_bounds__(BQ) void attn_f32_kernel(AttnParams p) {
     if (ref_rows && dec == DEC_REUSE) return;
     use_cache = dec != DEC_COMPUTE;
   }
-  const View& qv = ref_rows ? p.q_ref : p.q_tgt;
+  const View& qv = ref_rows ? (use_cache && p.q_cache.p ? p.q_cache : p.q_ref) : p.q_tgt;
   const View& ov = ref_rows ? p.o_ref : p.o_tgt;
   const int n_rows = ref_rows ? p.n_ref : p.n_tgt;
   const View& krv = use_cache ? p.k_cache : p.k_fresh;

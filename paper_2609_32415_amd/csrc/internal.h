@@ -34,6 +34,7 @@ struct SplitPlan {
 struct AttnParams {
   View q_tgt, k_tgt, v_tgt;
   View q_ref, k_fresh, v_fresh, k_cache, v_cache;
+  View q_cache;             // reference queries of the cached state; null p: q_ref serves
   View o_tgt, o_ref;        // written through const_cast
   float* mass_tgt;          // [B, H, n_tgt] or null
   float* lse_tgt;           // [B, H, n_tgt, 2] or null
@@ -99,9 +100,13 @@ hipError_t launch_q_change_gate(int dtype, int32_t B, int32_t H, int32_t n_tgt, 
                                 const float* theta, GateState* state, float* d_out, int32_t* decision_out,
                                 float* score_out, void* ws, hipStream_t stream);
 
-hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, View k_src,
-                               View v_src, View k_dst, View v_dst, const int32_t* decision, int32_t* age,
-                               int32_t step, hipStream_t stream);
+// Up to three (source, destination) pairs copied by one commit launch.
+struct CommitSet {
+  View src[3], dst[3];
+  int32_t n;
+};
+hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, CommitSet cs,
+                               const int32_t* decision, int32_t* age, int32_t step, hipStream_t stream);
 
 // Up to two [B, H, n, d] slice pairs whose relative change the diagnostics
 // reduce in one launch; chunks[] is filled by the launcher.

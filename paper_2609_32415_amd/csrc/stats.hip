@@ -5,7 +5,7 @@
 //               (Sec. 4 factorized-risk and depth-cutoff equations; Alg. 1)
 //   q_change_gate - both in two launches: every Q-change workgroup also sums the
 //               lagged mass over its rows; one workgroup then adds up and decides
-//   commit    - device-conditional refresh of a block's reference K/V cache
+//   commit    - device-conditional refresh of a block's cached reference state (K, V, Q)
 //
 // All are bandwidth- or latency-bound; they use 16-byte coalesced loads and
 // fixed-order reductions, so every result is bitwise reproducible.
@@ -212,29 +212,26 @@ __global__ __launch_bounds__(QG_THREADS) void q_change_gate_final(const float4* 
 
 constexpr int CC_THREADS = 256;
 
-__global__ __launch_bounds__(CC_THREADS) void cache_commit_kernel(View ks, View vs, View kd, View vd, int32_t H,
-                                                                  int32_t n_rows, int32_t vpr, int32_t esz,
-                                                                  const int32_t* decision, int32_t* age, int32_t step) {
+// Copies pair blockIdx.z of `cs` (source -> destination, [B, H, n_rows, d]) with 16-byte
+// vectors; exits at once unless the decision is COMPUTE (or absent).
+__global__ __launch_bounds__(CC_THREADS) void cache_commit_kernel(CommitSet cs, int32_t H, int32_t n_rows,
+                                                                  int32_t vpr, int32_t esz, const int32_t* decision,
+                                                                  int32_t* age, int32_t step) {
   if (decision && *decision != DEC_COMPUTE) return;
   const int bh = blockIdx.y;
   const int b = bh / H, h = bh - b * H;
+  const View src = cs.src[blockIdx.z], dst = cs.dst[blockIdx.z];
   const int64_t nvec = (int64_t)n_rows * vpr;
   const int vec = 16 / esz;
+  const char* sb = static_cast<const char*>(src.p) + (b * src.sb + h * src.sh) * esz;
+  char* db = static_cast<char*>(const_cast<void*>(dst.p)) + (b * dst.sb + h * dst.sh) * esz;
   for (int64_t v = (int64_t)blockIdx.x * CC_THREADS + threadIdx.x; v < nvec; v += (int64_t)gridDim.x * CC_THREADS) {
     const int64_t row = v / vpr;
     const int col = (int)(v % vpr) * vec;
-    const int64_t so_k = ((b * ks.sb + h * ks.sh) + row * ks.ss + col) * esz;
-    const int64_t so_v = ((b * vs.sb + h * vs.sh) + row * vs.ss + col) * esz;
-    const int64_t do_k = ((b * kd.sb + h * kd.sh) + row * kd.ss + col) * esz;
-    const int64_t do_v = ((b * vd.sb + h * vd.sh) + row * vd.ss + col) * esz;
-    const u32x4 xk = *reinterpret_cast<const u32x4*>(static_cast<const char*>(ks.p) + so_k);
-    *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(kd.p)) + do_k) = xk;
-    if (vs.p != nullptr) {  // null V views: copy K only
-      const u32x4 xv = *reinterpret_cast<const u32x4*>(static_cast<const char*>(vs.p) + so_v);
-      *reinterpret_cast<u32x4*>(static_cast<char*>(const_cast<void*>(vd.p)) + do_v) = xv;
-    }
+    const u32x4 x = *reinterpret_cast<const u32x4*>(sb + (row * src.ss + col) * esz);
+    *reinterpret_cast<u32x4*>(db + (row * dst.ss + col) * esz) = x;
   }
-  if (age && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) *age = step;
+  if (age && blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0 && threadIdx.x == 0) *age = step;
 }
 
 }  // namespace
@@ -295,17 +292,16 @@ hipError_t launch_q_change_gate(int dtype, int32_t B, int32_t H, int32_t n_tgt, 
                        decision_out, score_out);
 }
 
-hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, View k_src,
-                               View v_src, View k_dst, View v_dst, const int32_t* decision, int32_t* age,
-                               int32_t step, hipStream_t stream) {
+hipError_t launch_cache_commit(int dtype, int32_t B, int32_t H, int32_t n_ref, int32_t head_dim, CommitSet cs,
+                               const int32_t* decision, int32_t* age, int32_t step, hipStream_t stream) {
   const int esz = dtype == 0 ? 2 : 4;
   const int vpr = head_dim * esz / 16;
   const int64_t nvec = (int64_t)n_ref * vpr;
   int gx = (int)((nvec + CC_THREADS * 4 - 1) / (CC_THREADS * 4));
   if (gx < 1) gx = 1;
   if (gx > 1024) gx = 1024;
-  return launch_kernel(cache_commit_kernel, dim3(gx, B * H), dim3(CC_THREADS), 0, stream, k_src, v_src, k_dst, v_dst,
-                       H, n_ref, vpr, esz, decision, age, step);
+  return launch_kernel(cache_commit_kernel, dim3(gx, B * H, cs.n), dim3(CC_THREADS), 0, stream, cs, H, n_ref, vpr,
+                       esz, decision, age, step);
 }
 
 }  // namespace refadapt

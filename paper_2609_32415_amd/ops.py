@@ -76,6 +76,7 @@ def joint_attn(
     v_ref=None,
     k_cache=None,
     v_cache=None,
+    q_cache=None,
     qset="target",
     kvsrc="fresh",
     decision=None,
@@ -98,6 +99,10 @@ def joint_attn(
     workspace the library asks for (torch caching allocator), False runs
     without key splits, a uint8 device tensor is used as given (see
     ``attn_workspace``). Returns an ``AttnOut``.
+
+    ``q_cache``: reference queries of the cached state; reference queries that attend
+    over the cached K/V (``kvsrc="cache"`` with ``qset="all"``, or REACTIVATE under
+    ``kvsrc="device"``) read them instead of ``q_ref``.
 
     Reference segments (bf16): ``seg_end`` lists each segment's end row in R
     (multiples of 64 except the last, which is n_ref). With ``kvsrc="segments"``
@@ -178,6 +183,7 @@ def joint_attn(
         seg_end=(ctypes.c_int32 * L.RA_MAX_SEG)(*(list(seg_end or []) + [0] * (L.RA_MAX_SEG - n_seg))),
         seg_cache=cache_bits,
         seg_mass=None if smass_t is None else smass_t.data_ptr(),
+        q_cache=_view("q_cache", q_cache, dt, shp_r),
     )
     L.refadapt_joint_attn(desc, args, _stream())
     return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t, smass_t)
@@ -297,21 +303,25 @@ def q_change_gate(q_cur, q_prev, mass_prev, theta, state, block, step, mode="pro
     return d_out, decision_out, score_out
 
 
-def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0):
-    """Copy fresh reference K/V into the cache when ``decision`` is COMPUTE (or None);
-    with ``v_ref`` and ``v_cache`` None only K is copied."""
+def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0, q_ref=None, q_cache=None):
+    """Copy the fresh reference K, V (and Q when ``q_ref``/``q_cache`` are given) into the
+    cache when ``decision`` is COMPUTE (or None); with ``v_ref`` and ``v_cache`` None only K
+    is copied. One launch copies every pair."""
     B, H, n_ref, D = k_ref.shape
     dt = k_ref.dtype
     if (v_ref is None) != (v_cache is None):
         raise ValueError("v_ref and v_cache are both given or both None")
+    if (q_ref is None) != (q_cache is None):
+        raise ValueError("q_ref and q_cache are both given or both None")
     for name, t in (("decision", decision), ("age", age)):
         _on_gpu(name, t)
         if t is not None and t.dtype != torch.int32:
             raise ValueError(f"{name} must be int32")
     L.refadapt_cache_commit(
         B, H, n_ref, D, _DTYPES[dt],
-        _view("k_ref", k_ref, dt), _view("v_ref", v_ref, dt, k_ref.shape),
+        _view("k_ref", k_ref, dt), _view("v_ref", v_ref, dt, k_ref.shape), _view("q_ref", q_ref, dt, k_ref.shape),
         _view("k_cache", k_cache, dt, k_ref.shape), _view("v_cache", v_cache, dt, k_ref.shape),
+        _view("q_cache", q_cache, dt, k_ref.shape),
         _ptr(decision), _ptr(age), int(step), _stream(),
     )
 

@@ -26,9 +26,13 @@ video-editing shape, and a controller sweep):
 Key bias (bf16 workloads): per head h a random unit direction u_h is drawn;
 every reference key gets +0.5*sqrt(d)*u_h, and each target query's component
 along u_h is set to +1 in a seeded 30 % of target rows and to -lambda_h in
-the rest (lambda_h = 6h/(H-1), or drawn per block and head in ``sweep``).
-With the 1/sqrt(d) softmax scale this adds +0.5 or -0.5*lambda_h to that
-query's reference logits, so per-query reference mass spans about 0.05-0.65.
+the rest (lambda_h = 6h/(H-1)). With the 1/sqrt(d) softmax scale this adds
++0.5 or -0.5*lambda_h to that query's reference logits, so per-query reference
+mass spans about 0.05-0.65. In ``sweep`` lambda follows a depth profile: 6 at
+block 0 falling linearly to 0 at the deepest block, plus a seeded per-(block,
+head) offset uniform in [-1.5, 1.5], clipped to [0, 6]; the head-mean exposure
+then rises from about 0.24 to 0.5 with depth, so the head-mean score crosses a
+threshold at a depth that moves as the target change decays over the steps.
 """
 
 from __future__ import annotations
@@ -141,9 +145,20 @@ def sweep_tgt_drift(step, n_steps=8):
     return 0.3 + (0.05 - 0.3) * (step - 1) / (n_steps - 2)
 
 
+LAMBDA_JITTER = 1.5  # per-head spread of the sweep's key-bias depth profile
+
+
+def sweep_lambda_mean(block, n_blocks):
+    """Depth profile of the sweep's key bias: 6 at block 0, linear down to 0 at the
+    deepest block, so a target query's reference logits (and the head-mean exposure)
+    rise with depth."""
+    return 6.0 * (1.0 - block / (n_blocks - 1)) if n_blocks > 1 else 3.0
+
+
 def _lambda(w, block, h):
     if w.name == "sweep":
-        return float(_rng(w.seed, block, 0, ROLE_IDS["bias"], 1000 + h).uniform(0.0, 6.0))
+        jit = _rng(w.seed, block, 0, ROLE_IDS["bias"], 1000 + h).uniform(-LAMBDA_JITTER, LAMBDA_JITTER)
+        return float(min(6.0, max(0.0, sweep_lambda_mean(block, w.n_blocks) + jit)))
     return 6.0 * h / (w.heads - 1) if w.heads > 1 else 0.0
 
 

@@ -65,6 +65,13 @@ def _args(**kw):
         ({}, dict(v_ref=_t(ss=1 << 24)), L.RA_EUNSUPPORTED, "v_ref row stride"),
         (dict(batch=0), {}, L.RA_EINVAL, "batch"),
         ({}, dict(workspace=0x1008, workspace_bytes=1 << 20), L.RA_EUNSUPPORTED, "workspace"),
+        (dict(qset=L.RA_Q_ALL, kvsrc=L.RA_KV_CACHE), dict(k_cache=_t(), v_cache=_t(), o_ref=_t(),
+                                                          q_cache=_t(0x1002)), L.RA_EUNSUPPORTED, "q_cache"),
+        (dict(kvsrc=L.RA_KV_DEVICE), dict(k_cache=_t(), v_cache=_t(), q_ref=_t(), o_ref=_t(), decision=0x1000,
+                                          q_cache=_t(ss=132)), L.RA_EUNSUPPORTED, "q_cache"),
+        # q_ref stays required where the fresh K/V may be read by reference queries
+        (dict(kvsrc=L.RA_KV_DEVICE), dict(k_cache=_t(), v_cache=_t(), o_ref=_t(), decision=0x1000,
+                                          q_cache=_t()), L.RA_EINVAL, "q_ref"),
     ],
 )
 def test_joint_attn_rejects_bad_arguments(desc, args, status, msg):
@@ -122,10 +129,17 @@ def test_gate_and_commit_validation():
     assert L.LIB.refadapt_gate(1, 24, 4096, 0, 0, 9, p, p, p, p, p, p, None) == L.RA_EINVAL
     assert L.LIB.refadapt_gate(1, 24, 4096, -1, 0, 0, p, p, p, p, p, p, None) == L.RA_EINVAL
     assert L.LIB.refadapt_gate(1, 24, 4096, 0, 0, 0, None, p, p, p, p, p, None) == L.RA_EINVAL
-    assert L.LIB.refadapt_cache_commit(1, 2, 10, 128, L.RA_BF16, _t(), _t(), _t(0), _t(), None, None, 0, None) == L.RA_EINVAL
-    assert L.LIB.refadapt_cache_commit(1, 2, 10, 100, L.RA_BF16, _t(), _t(), _t(), _t(), None, None, 0, None) == L.RA_EUNSUPPORTED
+    cc = lambda n_ref=10, d=128, k=_t(), v=_t(), q=_t(0), kc=_t(), vc=_t(), qc=_t(0): L.LIB.refadapt_cache_commit(
+        1, 2, n_ref, d, L.RA_BF16, k, v, q, kc, vc, qc, None, None, 0, None)
+    assert cc(kc=_t(0)) == L.RA_EINVAL and "k_cache" in L.refadapt_last_error()
+    assert cc(k=_t(0), v=_t(0), vc=_t(0)) == L.RA_EINVAL and "k_ref" in L.refadapt_last_error()
+    # an optional pair with one side missing is an error
+    assert cc(q=_t()) == L.RA_EINVAL and "q_cache" in L.refadapt_last_error()
+    assert cc(vc=_t(0)) == L.RA_EINVAL and "v_cache" in L.refadapt_last_error()
+    assert cc(d=100) == L.RA_EUNSUPPORTED
+    assert cc(qc=_t(0x1002), q=_t()) == L.RA_EUNSUPPORTED and "q_cache" in L.refadapt_last_error()
     # Nothing to copy is not an error.
-    assert L.LIB.refadapt_cache_commit(1, 2, 0, 128, L.RA_BF16, _t(), _t(), _t(), _t(), None, None, 0, None) == L.RA_OK
+    assert cc(n_ref=0) == L.RA_OK
 
 
 def test_diagnostics_validation():
@@ -197,3 +211,4 @@ def test_segment_validation():
     a2 = args(2, [128, 300], mass=False, cache=1)
     a2.k_cache = _t(ss=256)
     assert call(seg(), a2) == L.RA_EUNSUPPORTED and "strides" in L.refadapt_last_error()
+

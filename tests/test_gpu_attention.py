@@ -305,8 +305,36 @@ def test_ragged_tiles_never_read_past_the_last_row(d, mode):
         assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
 
 
-FULL = [("single_ref", "target", "cache"), ("single_ref", "all", "fresh"), ("multi_ref", "target", "cache"),
-        ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"), ("video", "target", "cache"),
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+@pytest.mark.parametrize("kvsrc,decision", [("cache", None), ("device", 1), ("device", 2), ("fresh", None)],
+                         ids=["cache", "device-REACTIVATE", "device-COMPUTE", "fresh"])
+def test_cached_reference_queries(dtype, d, kvsrc, decision):
+    """q_cache (reference queries of the cached state) replaces q_ref exactly where reference
+    queries attend over the cached K/V: ALL/CACHE and REACTIVATE; COMPUTE and FRESH ignore it."""
+    print(f"q_cache {dtype} d{d} {kvsrc} {decision}", flush=True)
+    _, x = _inputs(dtype, d, 150, 190, 1, 2)
+    q_stale = synth.round_to_dtype(x["q_ref"] + 0.5 * np.random.default_rng(5).standard_normal(x["q_ref"].shape),
+                                   dtype)
+    t = {k: dev(v, dtype) for k, v in x.items()}
+    dec = None if decision is None else torch.tensor([decision], dtype=torch.int32, device="cuda:0")
+    got = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
+                         k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], q_cache=dev(q_stale, dtype),
+                         qset="all", kvsrc=kvsrc, decision=dec, ref_mass_refq=True)
+    torch.cuda.synchronize()
+    use_cache = kvsrc == "cache" or decision == 1
+    kr = x["k_ref_cache"] if use_cache else x["k_ref"]
+    vr = x["v_ref_cache"] if use_cache else x["v_ref"]
+    refr = joint_attention(q_stale if use_cache else x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
+    ref = joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"])
+    assert max_abs(host(got.o_ref), refr["o"]) <= O_TOL[dtype]
+    assert max_abs(host(got.ref_mass_refq), refr["ref_mass"]) <= MASS_TOL[dtype]
+    assert max_abs(host(got.o_tgt), ref["o"]) <= O_TOL[dtype]
+    assert max_abs(host(got.ref_mass), ref["ref_mass"]) <= MASS_TOL[dtype]
+
+
+FULL = [("single_ref", "target", "cache"), ("single_ref", "all", "fresh"), ("single_ref", "all", "cache"),
+        ("multi_ref", "target", "cache"), ("multi_ref", "all", "fresh"), ("multi_ref", "all", "cache"),
+        ("video", "target", "cache"), ("video", "all", "fresh"), ("video", "all", "cache"),
         ("ref8", "target", "cache"), ("ref8", "all", "fresh")]
 _FULL_CACHE = {}
 # eight 4096-token reference images plus 256 text tokens (the largest reference count swept)
@@ -338,10 +366,15 @@ def test_full_size_sampled_rows(name, qset, kvsrc):
     assert max_abs(host(got.ref_mass[:, :, rows]), ref["ref_mass"]) <= MASS_TOL["bf16"]
     m = host(got.ref_mass)
     assert np.all((m >= 0) & (m <= 1))
+    lse = host(got.lse[:, :, rows])
+    assert max_abs(lse[..., 0], ref["lse_ref"]) <= 1e-3 and max_abs(lse[..., 1], ref["lse_all"]) <= 1e-3
     if qset == "all":
         rr = synth.sample_rows(w.n_ref, 48, 4)
         refr = joint_attention(x["q_ref"][:, :, rr], kr, vr, x["k_tgt"], x["v_tgt"])
         assert max_abs(host(got.o_ref[:, :, rr]), refr["o"]) <= O_TOL["bf16"]
+        assert max_abs(host(got.ref_mass_refq[:, :, rr]), refr["ref_mass"]) <= MASS_TOL["bf16"]
+        mr = host(got.ref_mass_refq)
+        assert np.all((mr >= 0) & (mr <= 1))
 
 
 def _jump_inputs(d, pattern, n_ref=600, n_tgt=300, H=2, seed=11):

@@ -226,6 +226,20 @@ def test_cache_commit_k_only(decision, copied):
     assert torch.equal(dst, src) if copied else bool((dst == 0).all())
 
 
+@pytest.mark.parametrize("decision,copied", [(2, True), (0, False)])
+def test_cache_commit_with_queries(decision, copied):
+    """K, V and the reference queries of the state go to the cache in one launch."""
+    rng = np.random.default_rng(4)
+    shape = (2, 3, 130, 64)
+    src = [dev(rng.standard_normal(shape).astype(np.float32), "bf16") for _ in range(3)]
+    dst = [torch.zeros_like(x) for x in src]
+    dec = torch.tensor([decision], dtype=torch.int32, device="cuda:0")
+    ops.cache_commit(src[0], src[1], dst[0], dst[1], decision=dec, q_ref=src[2], q_cache=dst[2])
+    torch.cuda.synchronize()
+    for s_, d_ in zip(src, dst):
+        assert torch.equal(d_, s_) if copied else bool((d_ == 0).all())
+
+
 @pytest.mark.parametrize("decision,copied", [(2, True), (1, False), (0, False), (None, True)])
 def test_cache_commit(decision, copied):
     rng = np.random.default_rng(3)

@@ -121,6 +121,35 @@ def test_compute_blocks_match_full_fresh_and_refresh_cache_age():
     assert tr.ages[2].tolist() == [0, 2, 2, 2, 2, 2]
 
 
+def test_boundary_reference_rows_attend_with_the_cached_state_queries():
+    """Alg. 1 boundary branch: the restored reference state runs the reference-query
+    computation. Scale 1, d = 2, one head, 2 reference + 2 target rows, theta = 0, so step 1
+    reactivates block 0 and computes block 1. Reference keys (ln 5, 0) and (0, 0), target keys
+    zero; reference queries are 0 at step 0 and (1, 0) at step 1. The boundary's reference rows
+    therefore see all-zero logits (uniform attention): o = mean of [V_R(step 0); V_Y(step 1)] =
+    ((4,0) + (0,4) + (0,0) + (8,8)) / 4 = (3, 3). The computing block uses the current queries:
+    weights (5, 1, 1, 1) / 8, o = (5 (4,0) + (0,4) + (0,0) + (8,8)) / 8 = (3.5, 1.5)."""
+    ln5 = math.log(5.0)
+
+    def inputs(t, b):
+        return {
+            "q_ref": np.full((1, 1, 2, 2), 0.0) if t == 0 else np.tile([1.0, 0.0], (1, 1, 2, 1)),
+            "k_ref": np.array([[[[ln5, 0.0], [0.0, 0.0]]]]),
+            "v_ref": np.array([[[[4.0, 0.0], [0.0, 4.0]]]]) if t == 0 else np.array([[[[40.0, 0.0], [0.0, 40.0]]]]),
+            "q_tgt": np.array([[[[1.0, 2.0], [3.0, -1.0]]]]) * (1.0 + t),
+            "k_tgt": np.zeros((1, 1, 2, 2)),
+            "v_tgt": np.array([[[[1.0, 1.0], [1.0, 1.0]]]]) if t == 0 else np.array([[[[0.0, 0.0], [8.0, 8.0]]]]),
+        }
+
+    tr = run_controller(inputs, 2, 2, 0.0, scale=1.0, keep_outputs=True)
+    assert tr.decisions.tolist() == [[COMPUTE, COMPUTE], [REACTIVATE, COMPUTE]]
+    boundary = tr.outputs[(1, 0)]["o_all"][0, 0, :2]
+    np.testing.assert_allclose(boundary, [[3.0, 3.0], [3.0, 3.0]], rtol=0, atol=1e-14)
+    # the computing block reads this step's reference Q and V: V_R = 10 x the step-0 rows
+    computed = tr.outputs[(1, 1)]["o_all"][0, 0, :2]
+    np.testing.assert_allclose(computed, [[(5 * 40 + 8) / 8, (40 + 8) / 8]] * 2, rtol=0, atol=1e-13)
+
+
 def test_local_impact_closed_form():
     a = np.zeros((1, 1, 2, 2))
     b = np.zeros((1, 1, 2, 2))

@@ -77,3 +77,16 @@ def test_per_segment_key_bias_weights():
     with pytest.raises(ValueError):
         synth.base_tensors(synth.workload("tiny", n_ref=192, key_bias=True, ref_segments=(100,),
                                           ref_bias_weights=(1.0,)))
+
+
+def test_sweep_key_bias_depth_profile():
+    """The sweep's lambda falls with depth (6 at block 0 to 0 at the deepest block) with a bounded
+    per-head offset, so the head-mean reference exposure rises with depth."""
+    w = synth.workload("sweep")
+    lam = np.array([[synth._lambda(w, b, h) for h in range(w.heads)] for b in range(w.n_blocks)])
+    assert lam.min() >= 0.0 and lam.max() <= 6.0
+    mean = np.array([synth.sweep_lambda_mean(b, w.n_blocks) for b in range(w.n_blocks)])
+    assert mean[0] == 6.0 and mean[-1] == 0.0 and np.all(np.diff(mean) < 0)
+    inside = (mean[:, None] > synth.LAMBDA_JITTER) & (mean[:, None] < 6.0 - synth.LAMBDA_JITTER)
+    assert np.all(np.abs(lam - mean[:, None])[inside.repeat(w.heads, 1)] <= synth.LAMBDA_JITTER)
+    assert lam[:10].mean() > 4.0 and lam[-10:].mean() < 2.0
