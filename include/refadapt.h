@@ -266,6 +266,30 @@ ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, in
                                  size_t ws_bytes, void* stream);
 
 /*
+ * refadapt_q_change_gate_noalloc - refadapt_q_change_gate without a workspace.
+ *
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same computation
+ * and outputs as refadapt_q_change_gate (bitwise), with the per-chunk partial
+ * sums kept in a fixed 1 MiB device array of the library instead of a caller
+ * workspace. Nothing is allocated: each device holds its copy of that array
+ * from the library's load until the process ends; its address is looked up on
+ * the first call on a device. Calls on one device share the array, so calls
+ * that can overlap on a device (other streams, other threads) race and must be
+ * serialised by the caller. Contents need no initialisation (every call writes
+ * all the partials it reads).
+ * Errors: as refadapt_q_change_gate; RA_EUNSUPPORTED when the shape needs more
+ * than 1 MiB of partials (refadapt_q_change_gate_workspace_size > 1048576, e.g.
+ * batch*heads > 1024 with 64 chunks per head) or the device index is 64 or
+ * above; RA_ELAUNCH when the array's address cannot be obtained.
+ */
+ra_status refadapt_q_change_gate_noalloc(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim,
+                                         int32_t dtype, ra_tensor q_cur, ra_tensor q_prev, float eps, int32_t block,
+                                         int32_t step, int32_t mode, const float* mass_prev, const float* theta,
+                                         ra_gate_state* state, float* d_out, int32_t* decision_out,
+                                         float* score_out, void* stream);
+
+/*
  * refadapt_cache_commit - refresh a block's cached reference state.
  *
  * Copies k_ref -> k_cache, v_ref -> v_cache and q_ref -> q_cache

@@ -41,6 +41,7 @@ EXPORTED = (
     "refadapt_gate",
     "refadapt_q_change_gate_workspace_size",
     "refadapt_q_change_gate",
+    "refadapt_q_change_gate_noalloc",
     "refadapt_cache_commit",
     "refadapt_kv_drift_workspace_size",
     "refadapt_kv_drift",
@@ -142,6 +143,9 @@ def _load():
     lib.refadapt_q_change_gate.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, i32, i32, i32,
                                            vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.refadapt_q_change_gate.restype = i32
+    lib.refadapt_q_change_gate_noalloc.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, i32, i32,
+                                                   i32, vp, vp, vp, vp, vp, vp, vp]
+    lib.refadapt_q_change_gate_noalloc.restype = i32
     lib.refadapt_cache_commit.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, ra_tensor, ra_tensor,
                                           ra_tensor, ra_tensor, vp, vp, i32, vp]
     lib.refadapt_cache_commit.restype = i32
@@ -210,6 +214,13 @@ def refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, 
     return _check(LIB.refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block, step,
                                              mode, mass_prev, theta, state, d_out, decision_out, score_out,
                                              workspace, ws_bytes, stream))
+
+
+def refadapt_q_change_gate_noalloc(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block, step, mode,
+                                   mass_prev, theta, state, d_out, decision_out, score_out, stream):
+    return _check(LIB.refadapt_q_change_gate_noalloc(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block,
+                                                     step, mode, mass_prev, theta, state, d_out, decision_out,
+                                                     score_out, stream))
 
 
 def refadapt_cache_commit(batch, heads, n_ref, head_dim, dtype, k_ref, v_ref, q_ref, k_cache, v_cache, q_cache,

@@ -8,6 +8,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <algorithm>
+#include <mutex>
 #include <string>
 
 #include "refadapt.h"
@@ -410,6 +411,68 @@ ra_status refadapt_q_change_gate(int32_t batch, int32_t heads, int32_t n_tgt, in
                                             d_out, decision_out, score_out, workspace,
                                             static_cast<hipStream_t>(stream));
   return launch_status(e, "q_change_gate");
+}
+
+}  // extern "C"
+
+// ---- allocation-free Q-change + gate
+//
+// The fused Q-change + gate needs per-chunk partial sums between its two launches. This
+// variant keeps them in one fixed device array instead of a caller workspace, for callers
+// that cannot allocate. Each device holds its own copy of the array; host code takes its
+// device address once per device (hipGetSymbolAddress) and passes that address to the
+// kernels, never the array's name. Calls that overlap on one device share it and race.
+namespace {
+
+constexpr size_t kScratchBytes = size_t(1) << 20;  // 65536 partial records of 16 bytes
+constexpr int kMaxScratchDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// Device address of the current device's `scratch`, looked up on the first call per device.
+ra_status scratch_ptr(void** out) {
+  int dev = -1;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(RA_ELAUNCH, "q_change_gate_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(RA_EUNSUPPORTED, "q_change_gate_noalloc: device %d outside 0..%d", dev, kMaxScratchDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t r = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (r != hipSuccess || p == nullptr)
+      return fail(RA_ELAUNCH, "q_change_gate_noalloc: hipGetSymbolAddress(scratch): %s", hipGetErrorString(r));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return RA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ra_status refadapt_q_change_gate_noalloc(int32_t batch, int32_t heads, int32_t n_tgt, int32_t head_dim,
+                                         int32_t dtype, ra_tensor q_cur, ra_tensor q_prev, float eps, int32_t block,
+                                         int32_t step, int32_t mode, const float* mass_prev, const float* theta,
+                                         ra_gate_state* state, float* d_out, int32_t* decision_out,
+                                         float* score_out, void* stream) {
+  ra_status s;
+  if ((s = check_q_change_gate("q_change_gate_noalloc", batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps,
+                               block, step, mode, mass_prev, theta, state, d_out, decision_out, score_out)) != RA_OK)
+    return s;
+  const size_t need = refadapt_q_change_gate_workspace_size(batch, heads, n_tgt, head_dim);
+  if (need > kScratchBytes)
+    return fail(RA_EUNSUPPORTED,
+                "q_change_gate_noalloc: batch %d x heads %d x n_tgt %d x head_dim %d needs %zu bytes of partial sums; "
+                "the fixed scratch holds %zu (use refadapt_q_change_gate with a workspace)",
+                batch, heads, n_tgt, head_dim, need, kScratchBytes);
+  void* ws = nullptr;
+  if ((s = scratch_ptr(&ws)) != RA_OK) return s;
+  return refadapt_q_change_gate(batch, heads, n_tgt, head_dim, dtype, q_cur, q_prev, eps, block, step, mode,
+                                mass_prev, theta, state, d_out, decision_out, score_out, ws, kScratchBytes, stream);
 }
 
 ra_status refadapt_cache_commit(int32_t batch, int32_t heads, int32_t n_ref, int32_t head_dim, int32_t dtype,

@@ -303,6 +303,42 @@ def q_change_gate(q_cur, q_prev, mass_prev, theta, state, block, step, mode="pro
     return d_out, decision_out, score_out
 
 
+def q_change_gate_noalloc(q_cur, q_prev, mass_prev, theta, state, block, step, mode="product", eps=1e-8, d_out=None,
+                          decision_out=None, score_out=None):
+    """``q_change_gate`` through ``refadapt_q_change_gate_noalloc``: no workspace, the library's
+    fixed device scratch holds the partial sums (for callers that cannot allocate; calls that
+    overlap on one device race). Outputs must be passed in to allocate nothing here either."""
+    B, H, n, D = q_cur.shape
+    dt = q_cur.dtype
+    if dt not in _DTYPES:
+        raise ValueError(f"unsupported dtype {dt}")
+    dev = q_cur.device
+    if d_out is None:
+        d_out = torch.empty((B, H), dtype=torch.float32, device=dev)
+    if decision_out is None:
+        decision_out = torch.empty(1, dtype=torch.int32, device=dev)
+    if score_out is None:
+        score_out = torch.empty(3, dtype=torch.float32, device=dev)
+    for name, t in (("mass_prev", mass_prev), ("theta", theta), ("state", state), ("d_out", d_out),
+                    ("decision_out", decision_out), ("score_out", score_out)):
+        _on_gpu(name, t)
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if tuple(mass_prev.shape) != (B, H, n) or mass_prev.dtype != torch.float32:
+        raise ValueError("mass_prev must be fp32 [B, H, n_tgt]")
+    if theta.dtype != torch.float32 or state.dtype != torch.int32 or state.numel() != 4:
+        raise ValueError("theta must be fp32 and state int32[4]")
+    need = 2 * (block + 1) if mode == "and" else block + 1
+    if theta.numel() < need:
+        raise ValueError(f"theta has {theta.numel()} entries; block {block} needs {need}")
+    L.refadapt_q_change_gate_noalloc(
+        B, H, n, D, _DTYPES[dt], _view("q_cur", q_cur, dt), _view("q_prev", q_prev, dt, q_cur.shape), float(eps),
+        int(block), int(step), _GATE[mode], _ptr(mass_prev), _ptr(theta), _ptr(state), _ptr(d_out),
+        _ptr(decision_out), _ptr(score_out), _stream(),
+    )
+    return d_out, decision_out, score_out
+
+
 def cache_commit(k_ref, v_ref, k_cache, v_cache, decision=None, age=None, step=0, q_ref=None, q_cache=None):
     """Copy the fresh reference K, V (and Q when ``q_ref``/``q_cache`` are given) into the
     cache when ``decision`` is COMPUTE (or None); with ``v_ref`` and ``v_cache`` None only K

@@ -212,3 +212,17 @@ def test_segment_validation():
     a2.k_cache = _t(ss=256)
     assert call(seg(), a2) == L.RA_EUNSUPPORTED and "strides" in L.refadapt_last_error()
 
+
+def test_q_change_gate_noalloc_validation():
+    """Argument checks and the scratch limit are host-side: nothing reaches a device."""
+    p = ctypes.c_void_p(0x1000)
+    call = lambda B=1, H=24, n=4096, d=128, mode=0, m=p: L.LIB.refadapt_q_change_gate_noalloc(
+        B, H, n, d, L.RA_BF16, _t(), _t(), 1e-8, 0, 1, mode, m, p, p, p, p, p, None)
+    assert call(B=0) == L.RA_EINVAL and "q_change_gate_noalloc" in L.refadapt_last_error()
+    assert call(m=None) == L.RA_EINVAL
+    assert call(mode=7) == L.RA_EINVAL
+    assert call(d=100) == L.RA_EUNSUPPORTED
+    # 2048 heads x 64 chunks x 16 bytes = 2 MiB of partials: beyond the fixed 1 MiB scratch
+    assert L.refadapt_q_change_gate_workspace_size(1, 2048, 4096, 128) == 1 << 20  # 32 chunks: fits
+    assert L.refadapt_q_change_gate_workspace_size(1, 2048, 8192, 128) == 2 << 20
+    assert call(H=2048, n=8192) == L.RA_EUNSUPPORTED and "fixed scratch" in L.refadapt_last_error()

@@ -1,0 +1,51 @@
+"""The allocation-free fused Q-change + gate (refadapt_q_change_gate_noalloc) against the
+workspace entry point (refadapt_q_change_gate) on the same inputs: D, the decision, the scores
+and the gate state must be bitwise the same. Two calls in a row, the second smaller than the
+first, so the second reads the library's scratch after the first left its partials there."""
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_32415_amd import ops
+
+pytestmark = pytest.mark.gpu
+
+CALLS = [
+    # (B, H, n_tgt, head_dim, dtype, mode, block, step, theta)
+    (1, 24, 4096, 128, torch.bfloat16, "product", 0, 1, 0.02),
+    (2, 3, 333, 64, torch.bfloat16, "and", 1, 2, (0.1, 0.2)),
+    (1, 2, 256, 64, torch.float32, "product", 0, 3, 0.5),
+]
+
+
+def _inputs(B, H, n, d, dtype, seed):
+    g = torch.Generator(device="cuda:0")
+    g.manual_seed(seed)
+    q_prev = torch.randn((B, H, n, d), generator=g, device="cuda:0").to(dtype)
+    q_cur = (q_prev.float() + 0.3 * torch.randn((B, H, n, d), generator=g, device="cuda:0")).to(dtype)
+    mass = torch.rand((B, H, n), generator=g, device="cuda:0")
+    return q_cur, q_prev, mass
+
+
+def _run(fn, q_cur, q_prev, mass, theta, mode, block, step, **kw):
+    state = ops.new_gate_state("cuda:0")
+    d, dec, sc = fn(q_cur, q_prev, mass, theta, state, block, step, mode, **kw)
+    torch.cuda.synchronize()
+    return d.cpu(), dec.cpu(), sc.cpu(), state.cpu()
+
+
+def test_noalloc_matches_workspace_entry_point_on_consecutive_calls():
+    for i, (B, H, n, d, dtype, mode, block, step, theta) in enumerate(CALLS):
+        print(f"noalloc call {i}: B{B} H{H} n{n} d{d} {dtype} {mode}", flush=True)
+        q_cur, q_prev, mass = _inputs(B, H, n, d, dtype, 100 + i)
+        th = torch.tensor(np.repeat(np.asarray(theta, dtype=np.float32)[None], block + 1, 0).ravel(),
+                          device="cuda:0")
+        ref = _run(ops.q_change_gate, q_cur, q_prev, mass, th, mode, block, step)
+        out = _run(ops.q_change_gate_noalloc, q_cur, q_prev, mass, th, mode, block, step,
+                   d_out=torch.empty((B, H), dtype=torch.float32, device="cuda:0"),
+                   decision_out=torch.empty(1, dtype=torch.int32, device="cuda:0"),
+                   score_out=torch.empty(3, dtype=torch.float32, device="cuda:0"))
+        for a, b in zip(out, ref):
+            assert torch.equal(a, b), (i, a, b)
+        assert torch.isfinite(out[0]).all() and float(out[0].max()) > 0.0
