@@ -1,28 +1,33 @@
 """Benchmark of the RefAdapt-DiT joint-attention hot path on one MI355X.
 
-One step = one pass of the whole path over one block of the multi-reference
+One step = one denoising step of Alg. 1 over three blocks of the multi-reference
 image-editing workload (batch 1, 24 heads, head_dim 128, 4096 target tokens,
-3 x 4096 reference-image + 256 text tokens = 12544 reference tokens, bf16):
+3 x 4096 reference-image + 256 text tokens = 12544 reference tokens, bf16),
+executed by the on-device controller exactly as in a trajectory. Per-block
+thresholds (inf, 0, 0) make the three blocks take the three decisions:
 
-  1+2. Q-change and gate, one launch:
-                   D = ||Q_t - Q_{t-1}||_F / (||Q_{t-1}||_F + eps) per head, then the
-                   head-mean D*M against theta, decision written on the device
-  3. reuse attn    target queries over [cached K_R; K_Y]      (0.838 TFLOP)
-  4. full attn     all queries over [fresh K_R; K_Y]          (3.402 TFLOP)
-  5. cache commit  fresh reference K/V -> cache if the decision is COMPUTE
+  block 0  Q-change + gate -> REUSE: target queries over [cached K_R; K_Y]    (0.838 TFLOP)
+  block 1  Q-change + gate -> REACTIVATE (the boundary): target queries and the
+           cached reference queries over [cached K_R; K_Y]                    (3.402 TFLOP)
+  block 2  Q-change + gate -> COMPUTE: all queries over [fresh K_R; K_Y], then
+           the commit copies the fresh reference Q/K/V into the block cache   (3.402 TFLOP)
 
-``value`` = attention FLOPs of (3)+(4) / measured step time (TFLOP/s). The
-JSON line also carries each attention mode on its own, the attention-time
-speedup of a reused block over a computed one, the roofline of the dominant
-kernel (the full-fresh attention) measured live with HIP events on the launch
-stream, and the fp64 CPU oracle timed on a bounded sample of the same work.
+Every launch reads its decision word on the device (no host round-trip).
+``value`` = attention FLOPs of the three blocks / measured step time. The JSON
+line also carries each phase's mean / median / min, each attention mode on its
+own, the mean shader clock over the COMPUTE block's attention launches (an
+in-kernel probe) and the fraction of peak at that clock, the roofline of the
+dominant kernel (the COMPUTE block's attention) measured live with HIP events
+on the launch stream, the Q-change at the multi-reference and video sizes, one
+depth-adaptive controller trajectory against its full-fresh trajectory
+(60 blocks x 8 steps, single-reference shapes: the attention-time speedup of
+adaptive reuse), and the fp64 CPU oracle timed on a bounded sample.
 
-``--sweep`` additionally runs the 60-block x 8-step controller sweep
-(single-reference shapes, 3 x 3 thresholds, cue ablation, graph replays) and
-reports the reuse fraction, the attention-time speedup of adaptive reuse and
-the output error against a full-fresh trajectory. ``--ref-sweep`` runs the
-reference-count sweep (1..8 reference images). ``--shapes`` times the reuse and
-full-fresh attention at the single-reference, multi-reference and video shapes.
+``--sweep`` runs the whole controller sweep (3 x 3 thresholds, cue ablation,
+graph replays), ``--ref-sweep`` the reference-count sweep (1..8 reference
+images), ``--shapes`` times reuse, REACTIVATE and full-fresh attention at every
+workload shape (and at one GPU's share of an 8-way head split), ``--segments``
+the per-reference exposure table, ``--diagnostics`` the sidecar trajectory.
 """
 
 from __future__ import annotations
@@ -107,43 +112,92 @@ def _traffic_from_profile():
 
 
 def time_shapes(dev, reps=10):
-    """Reuse (target queries, cached K/V) and full-fresh (all queries, fresh K/V) attention at
-    the single-reference, multi-reference and video workload shapes, seeded synthetic inputs
-    (the fresh reference K/V stand in for the cache), event-timed over ``reps`` launches after
-    warm-up."""
+    """Reuse (target queries over the cached K/V), REACTIVATE (all queries over the cached K/V,
+    the reference rows with the cached queries) and full-fresh (all queries over fresh K/V)
+    attention at the single-reference, multi-reference and video workload shapes, and at the
+    multi-reference shape with 3 heads (one GPU's share when 24 heads are split over 8 GPUs);
+    seeded synthetic inputs, the stale cache of each workload, event-timed over ``reps``
+    launches after warm-up."""
     import torch
 
     from paper_2609_32415_amd import ops, synth
     from paper_2609_32415_amd.controller import time_launches
 
     rows = []
-    for name in ("single_ref", "multi_ref", "video"):
-        w = synth.workload(name)
+    for name, over in (("single_ref", {}), ("multi_ref", {}), ("video", {}), ("multi_ref", {"heads": 3})):
+        w = synth.workload(name, **over)
         x = synth.block_inputs(w)
+        x.update({f"{k}_cache": v for k, v in synth.stale_cache(w, x).items()})
         bf = lambda a: torch.from_numpy(a).to(dev).to(torch.bfloat16)
-        t = {k: bf(x[k]) for k in ("q_tgt", "k_tgt", "v_tgt", "q_ref", "k_ref", "v_ref")}
+        t = {k: bf(v) for k, v in x.items()}
         B, H, n_tgt, D = t["q_tgt"].shape
         n_ref = t["k_ref"].shape[2]
         ws_r = ops.attn_workspace(t["q_tgt"], n_ref, "target", "cache")
+        ws_a = ops.attn_workspace(t["q_tgt"], n_ref, "all", "cache")
         ws_f = ops.attn_workspace(t["q_tgt"], n_ref, "all", "fresh")
+        f_tgt, f_all = attn_flops(H, n_tgt, n_ref + n_tgt, D, B), attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, D, B)
         calls = {
-            "reuse": (lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=t["k_ref"], v_cache=t["v_ref"],
-                                             n_ref=n_ref, qset="target", kvsrc="cache", workspace=ws_r),
-                      attn_flops(H, n_tgt, n_ref + n_tgt, D, B)),
+            "reuse": (lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=t["k_ref_cache"],
+                                             v_cache=t["v_ref_cache"], n_ref=n_ref, qset="target", kvsrc="cache",
+                                             workspace=ws_r), f_tgt),
+            "reactivate": (lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"],
+                                                  k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"],
+                                                  q_cache=t["q_ref"], qset="all", kvsrc="cache", workspace=ws_a),
+                           f_all),
             "full_fresh": (lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"],
-                                                  v_ref=t["v_ref"], qset="all", kvsrc="fresh", workspace=ws_f),
-                           attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, D, B)),
+                                                  v_ref=t["v_ref"], qset="all", kvsrc="fresh", workspace=ws_f), f_all),
         }
-        row = {"workload": name, "heads": H, "head_dim": D, "n_ref": n_ref, "n_tgt": n_tgt}
+        row = {"workload": name + (f"_h{H}" if over else ""), "heads": H, "head_dim": D, "n_ref": n_ref,
+               "n_tgt": n_tgt}
         for mode, (fn, flop) in calls.items():
             ms = time_launches(fn, reps=reps)
             tf = flop / (ms * 1e-3) / 1e12
             row[mode] = {"ms": round(ms, 4), "tflops": round(tf, 2), "pct_peak": round(100 * tf / BF16_PEAK_TFLOPS, 2)}
         rows.append(row)
-        print(f"shape {name}: reuse {row['reuse']}, full-fresh {row['full_fresh']}", file=sys.stderr, flush=True)
+        print(f"shape {row['workload']}: reuse {row['reuse']}, reactivate {row['reactivate']}, "
+              f"full-fresh {row['full_fresh']}", file=sys.stderr, flush=True)
         del t, x
         torch.cuda.empty_cache()
     return rows
+
+
+def host_info():
+    """CPU model, core counts and the BLAS library numpy uses (for the oracle baseline)."""
+    import platform
+
+    import numpy as np  # noqa: F401  (loads the BLAS so threadpoolctl can see it)
+
+    model, sockets, cores_per_socket = platform.processor() or None, None, None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+        ids = set()
+        for block in open("/proc/cpuinfo").read().split("\n\n"):
+            phys = core = None
+            for line in block.splitlines():
+                if line.startswith("physical id"):
+                    phys = line.split(":", 1)[1].strip()
+                elif line.startswith("core id"):
+                    core = line.split(":", 1)[1].strip()
+            if core is not None:
+                ids.add((phys, core))
+        physical = len(ids) or None
+    except OSError:
+        physical = None
+    blas = None
+    try:
+        from threadpoolctl import threadpool_info
+
+        libs = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if libs:
+            i = libs[0]
+            blas = {"internal_api": i.get("internal_api"), "version": i.get("version"),
+                    "library": os.path.basename(i.get("filepath") or ""), "threads": i.get("num_threads")}
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "physical_cores": physical, "blas": blas}
 
 
 def cpu_baseline(x, seconds):
@@ -153,12 +207,8 @@ def cpu_baseline(x, seconds):
 
     from oracle import joint_attention
 
-    try:
-        from threadpoolctl import threadpool_info
-
-        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count()
+    info = host_info()
+    threads = (info["blas"] or {}).get("threads") or 1
     H, n_ref, n_tgt, d = x["q_ref"].shape[1], x["k_ref"].shape[2], x["k_tgt"].shape[2], x["q_tgt"].shape[3]
     rows, spent, total_rows = 8, 0.0, 0
     q_all = np.concatenate([x["q_ref"], x["q_tgt"]], axis=2)
@@ -171,14 +221,25 @@ def cpu_baseline(x, seconds):
         total_rows += rows
         rows = min(rows * 2, 512)
     flops = attn_flops(H, total_rows, n_ref + n_tgt, d)
+    rate = flops / spent
+    full = attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, d)
     return {
-        "value": round(flops / spent / 1e12, 6),
+        "value": round(rate / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": threads,
         "kind": "oracle",
         "sample": f"full-fresh joint attention of {total_rows} sampled query rows x {H} heads over all "
-        f"{n_ref + n_tgt} keys (fp64 numpy oracle, {spent:.1f} s)",
+        f"{n_ref + n_tgt} keys (fp64 numpy oracle, {spent:.1f} s); the whole full-fresh launch would take "
+        f"{full / rate:.0f} s at this rate",
+        "host": info,
     }
+
+
+def _stats(v):
+    import numpy as np
+
+    v = np.asarray(v, dtype=np.float64)
+    return {"mean": float(v.mean()), "median": float(np.median(v)), "min": float(v.min())}
 
 
 def main():
@@ -199,85 +260,79 @@ def main():
     import torch
 
     from paper_2609_32415_amd import ops, synth
+    from paper_2609_32415_amd.controller import Controller
 
     dev = torch.device("cuda:0")
+    log = lambda m: print(m, file=sys.stderr, flush=True)
     w = synth.workload(WORKLOAD, ref_drift=0.01, tgt_drift=0.3, n_steps=2)
     tr = synth.Trajectory(w)
-    x0 = tr.step_tensors(0)  # previous step: cache contents and previous target Q
-    x1 = tr.step_tensors(1)  # current step: fresh tensors
+    x0 = tr.step_tensors(0)  # previous step
+    x1 = tr.step_tensors(1)  # current step
     bf = lambda a: torch.from_numpy(a).to(dev).to(torch.bfloat16)
-    t = {k: bf(v) for k, v in x1.items()}
-    cache_k, cache_v, q_prev = bf(x0["k_ref"]), bf(x0["v_ref"]), bf(x0["q_tgt"])
-    B, H, n_tgt, D = t["q_tgt"].shape
-    n_ref = t["k_ref"].shape[2]
+    set0 = {k: bf(v) for k, v in x0.items()}
+    set1 = {k: bf(v) for k, v in x1.items()}
+    B, H, n_tgt, D = set1["q_tgt"].shape
+    n_ref = set1["k_ref"].shape[2]
 
-    # Lagged per-query mass from the previous step's executed (full) attention.
-    mass_prev = ops.joint_attn(bf(x0["q_tgt"]), bf(x0["k_tgt"]), bf(x0["v_tgt"]), k_ref=cache_k, v_ref=cache_v).ref_mass
-    theta = torch.full((1,), 0.1 * 0.2, dtype=torch.float32, device=dev)
-    state = ops.new_gate_state(dev)
-    ws = ops.q_change_workspace(t["q_tgt"])
-    ws_qg = ops.q_change_gate_workspace(t["q_tgt"])
-    d_out = torch.empty((B, H), dtype=torch.float32, device=dev)
-    dec = torch.empty(1, dtype=torch.int32, device=dev)
-    score = torch.empty(3, dtype=torch.float32, device=dev)
-    o_tgt_r = torch.empty_like(t["q_tgt"])
-    o_tgt_f = torch.empty_like(t["q_tgt"])
-    o_ref_f = torch.empty_like(t["q_ref"])
-    mass_r = torch.empty((B, H, n_tgt), dtype=torch.float32, device=dev)
-    mass_f = torch.empty((B, H, n_tgt), dtype=torch.float32, device=dev)
-    commit_k, commit_v = cache_k.clone(), cache_v.clone()
-    # Key-split workspaces (partial rows of the query tiles of a last, partly filled round).
-    ws_r = ops.attn_workspace(t["q_tgt"], n_ref, "target", "cache")
-    ws_f = ops.attn_workspace(t["q_tgt"], n_ref, "all", "fresh")
-
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-    marks = {k: [] for k in ("qcg", "reuse", "full", "commit")}
-
-    def step(record):
-        e = [ev() for _ in range(5)] if record else None
-        if record:
-            e[0].record()
-        ops.q_change_gate(t["q_tgt"], q_prev, mass_prev, theta, state, 0, 1, "product", d_out=d_out,
-                          decision_out=dec, score_out=score, workspace=ws_qg)
-        if record:
-            e[1].record()
-        ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_cache=cache_k, v_cache=cache_v, n_ref=n_ref,
-                       qset="target", kvsrc="cache", o_tgt=o_tgt_r, ref_mass=mass_r, workspace=ws_r)
-        if record:
-            e[2].record()
-        ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"], v_ref=t["v_ref"],
-                       qset="all", kvsrc="fresh", o_tgt=o_tgt_f, o_ref=o_ref_f, ref_mass=mass_f, workspace=ws_f)
-        if record:
-            e[3].record()
-        ops.cache_commit(t["k_ref"], t["v_ref"], commit_k, commit_v, decision=dec)
-        if record:
-            e[4].record()
-        return e
-
-    for _ in range(args.warmup):
-        step(False)
+    # ---- the timed step: Alg. 1 over three blocks (REUSE, REACTIVATE, COMPUTE)
+    NB = 3
+    ctl = Controller(NB, 2, B, H, n_ref, n_tgt, D, (math.inf, 0.0, 0.0), device=dev)
+    ctl.step(0, [set0] * NB)  # step 0: every block computes, caches and records
     torch.cuda.synchronize()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    probe = {"reuse": torch.zeros(2, dtype=torch.int64, device=dev),
+             "full": torch.zeros(2, dtype=torch.int64, device=dev)}
+    sets = (set1, set0)
+
+    def step(i, record):
+        evs = []
+        mark = (lambda name: evs.append(ev()) or evs[-1].record()) if record else None
+        if record:
+            mark("start")
+        xs = [sets[i % 2]] * NB
+        for b in range(NB):
+            cp = probe["reuse"] if (record and b == 0) else probe["full"] if (record and b == 2) else None
+            ctl.block(1, b, xs[b], mark=mark, clock_probe=cp)
+        return evs
+
+    for i in range(args.warmup):
+        step(i, False)
+    torch.cuda.synchronize()
+    dec = ctl.decisions[1].cpu().tolist()
+    assert dec == [ops.REUSE, ops.REACTIVATE, ops.COMPUTE], f"bench step decisions {dec}"
+    for v in probe.values():
+        v.zero_()
     t0, t1 = ev(), ev()
     pending = []
     torch.cuda.synchronize()
     t0.record()
-    for _ in range(args.steps):
-        pending.append(step(True))
+    for i in range(args.steps):
+        pending.append(step(args.warmup + i, True))  # the input sets keep alternating
     t1.record()
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
-    for e in pending:
-        for k, (a, b) in zip(marks, zip(e[:-1], e[1:])):
-            marks[k].append(a.elapsed_time(b))
-    ms = {k: float(np.mean(v)) for k, v in marks.items()}
     ms_per_step = total_ms / args.steps
+    assert ctl.decisions[1].cpu().tolist() == [ops.REUSE, ops.REACTIVATE, ops.COMPUTE]
+    # phases: per block gate, attn, commit (events 1 + 3 b + k)
+    phase = {}
+    names = ["gate", "attn", "commit"]
+    for e in pending:
+        for b in range(NB):
+            for k, nm in enumerate(names):
+                a_, b_ = e[3 * b + k], e[3 * b + k + 1]
+                phase.setdefault(f"b{b}_{nm}", []).append(a_.elapsed_time(b_))
+    st = {k: _stats(v) for k, v in phase.items()}
+    ms_reuse, ms_react, ms_full = st["b0_attn"]["mean"], st["b1_attn"]["mean"], st["b2_attn"]["mean"]
+    cyc = probe["full"].cpu().tolist()
+    sclk_mhz = 100.0 * cyc[0] / cyc[1] if cyc[1] > 0 else None
+    cyc_r = probe["reuse"].cpu().tolist()
+    sclk_reuse_mhz = 100.0 * cyc_r[0] / cyc_r[1] if cyc_r[1] > 0 else None
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
+    log(f"bench step: {ms_per_step:.4f} ms; reuse {ms_reuse:.4f}, reactivate {ms_react:.4f}, compute {ms_full:.4f} ms; "
+        f"sclk {sclk_mhz}")
 
-    # Outside the timed step: the separate Q-change and gate kernels the fused launch replaces,
-    # and the diagnostics. Two figures each:
-    #  * cold: one launch between events after a 512 MiB read (a reduction, so no dirty lines
-    #    are left to write back) has evicted its inputs from the 256 MB last-level cache;
-    #  * hot: n back-to-back launches replayed from a captured HIP graph (device time per
-    #    launch with the inputs cache-resident; no host launch gaps).
+    # ---- outside the timed step: the small kernels, cold (inputs evicted from the
+    # last-level cache by a 512 MiB read) and hot (back-to-back graph replay)
     flush = torch.ones(128 << 20, dtype=torch.float32, device=dev)
 
     def timed(fn, n=20):
@@ -292,7 +347,7 @@ def main():
             b.record()
             pairs.append((a, b))
         torch.cuda.synchronize()
-        return float(np.mean([a.elapsed_time(b) for a, b in pairs]))
+        return _stats([a.elapsed_time(b) for a, b in pairs])
 
     def timed_hot(fn, n=20):
         torch.cuda.synchronize()
@@ -309,43 +364,62 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / n
 
-    def qcg():
-        ops.q_change_gate(t["q_tgt"], q_prev, mass_prev, theta, state, 0, 1, "product", d_out=d_out,
-                          decision_out=dec, score_out=score, workspace=ws_qg)
-
-    def qc():
-        ops.q_change(t["q_tgt"], q_prev, out=d_out, workspace=ws)
-
-    def gate():
-        ops.gate(d_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec, score_out=score)
-
-    ms["qcg_hot"] = timed_hot(qcg)
-    ms["qc"], ms["qc_hot"] = timed(qc), timed_hot(qc)
-    ms["gate"], ms["gate_hot"] = timed(gate), timed_hot(gate)
-    # The cache commit of a computed block: copies the fresh reference K/V into the cache.
-    ms["commit_copy"] = timed(lambda: ops.cache_commit(t["k_ref"], t["v_ref"], commit_k, commit_v))
-
-    # Diagnostics sidecar kernels (read-only probes), at the same shapes.
-    ws_kv = ops.kv_drift_workspace(t["k_ref"])
-    ws_ratio = ops.drift_log_ratio_workspace(t["k_ref"], t["k_tgt"])
-    ws_imp = ops.output_impact_workspace(o_tgt_r)
-    diag_out = torch.empty((3, B, H), dtype=torch.float32, device=dev)
-    ms["kv_drift"] = timed(lambda: ops.kv_drift(t["k_ref"], cache_k, t["v_ref"], cache_v, d_k=diag_out[0],
-                                                d_v=diag_out[1], e_kv=diag_out[2], workspace=ws_kv))
-    k_prev_tgt = bf(x0["k_tgt"])
-    ms["ratio"] = timed(lambda: ops.drift_log_ratio(t["k_ref"], cache_k, t["k_tgt"], k_prev_tgt, d_ref=diag_out[0],
-                                                    d_tgt=diag_out[1], rho=diag_out[2], workspace=ws_ratio))
-    ms["impact"] = timed(lambda: ops.output_impact(o_tgt_r, o_tgt_f, out=diag_out[0], workspace=ws_imp))
-    ms["mass_mean"] = timed(lambda: ops.mass_mean(mass_f, out=diag_out[0]))
-    diag_bytes = {"kv_drift": 4 * B * H * n_ref * D * 2, "ratio": 2 * B * H * (n_ref + n_tgt) * D * 2,
-                  "impact": 2 * B * H * n_tgt * D * 2, "mass_mean": B * H * n_tgt * 4}
+    small = {}
+    theta = torch.full((1,), 0.1 * 0.2, dtype=torch.float32, device=dev)
+    state = ops.new_gate_state(dev)
+    d_out = torch.empty((B, H), dtype=torch.float32, device=dev)
+    dec_out = torch.empty(1, dtype=torch.int32, device=dev)
+    score = torch.empty(3, dtype=torch.float32, device=dev)
+    for name, over in (("multi_ref", {}), ("video", {})):
+        if name == "video":
+            wv = synth.workload("video")
+            g = torch.Generator(device=dev)
+            g.manual_seed(wv.seed)
+            q_prev = torch.randn((1, wv.heads, wv.n_tgt, wv.head_dim), generator=g, device=dev).to(torch.bfloat16)
+            q_cur = (q_prev.float() + wv.tgt_drift * torch.randn(q_prev.shape, generator=g, device=dev)).to(torch.bfloat16)
+            mass_prev = torch.rand((1, wv.heads, wv.n_tgt), generator=g, device=dev)
+        else:
+            q_cur, q_prev, mass_prev = set1["q_tgt"], set0["q_tgt"], ctl.recorded_mass(0)
+        bq, hq, nq, dq = q_cur.shape
+        ws_qc = ops.q_change_workspace(q_cur)
+        ws_qg = ops.q_change_gate_workspace(q_cur)
+        dq_out = torch.empty((bq, hq), dtype=torch.float32, device=dev)
+        qc_bytes = 2 * q_cur.numel() * 2
+        qcg_bytes = qc_bytes + mass_prev.numel() * 4
+        qc = lambda: ops.q_change(q_cur, q_prev, out=dq_out, workspace=ws_qc)
+        qcg = lambda: ops.q_change_gate(q_cur, q_prev, mass_prev, theta, state, 0, 1, "product", d_out=dq_out,
+                                        decision_out=dec_out, score_out=score, workspace=ws_qg)
+        gt = lambda: ops.gate(dq_out, mass_prev, theta, state, 0, 1, "product", decision_out=dec_out,
+                              score_out=score)
+        r = {"bytes_q_change": qc_bytes, "bytes_q_change_gate": qcg_bytes}
+        for key, fn, nbytes in (("q_change", qc, qc_bytes), ("q_change_gate", qcg, qcg_bytes),
+                                ("gate", gt, mass_prev.numel() * 4 + bq * hq * 4)):
+            cold = timed(fn)
+            r[key] = {"cold_us": round(cold["mean"] * 1e3, 2), "cold_median_us": round(cold["median"] * 1e3, 2),
+                      "cold_min_us": round(cold["min"] * 1e3, 2),
+                      "cold_gbs": round(nbytes / (cold["mean"] * 1e-3) / 1e9, 1),
+                      "hot_us": round(timed_hot(fn) * 1e3, 2)}
+            r[key]["hot_gbs"] = round(nbytes / (r[key]["hot_us"] * 1e-6) / 1e9, 1)
+        small[name] = r
+        log(f"small kernels at {name}: {r}")
+    del flush
 
     f_reuse = attn_flops(H, n_tgt, n_ref + n_tgt, D, B)
     f_full = attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, D, B)
-    value = (f_reuse + f_full) / (ms_per_step * 1e-3) / 1e12
-    qc_bytes = 2 * B * H * n_tgt * D * 2
-    full_tflops = f_full / (ms["full"] * 1e-3) / 1e12
-    reuse_tflops = f_reuse / (ms["reuse"] * 1e-3) / 1e12
+    value = (f_reuse + 2 * f_full) / (ms_per_step * 1e-3) / 1e12
+    tfl = lambda f, ms: f / (ms * 1e-3) / 1e12
+    full_tflops = tfl(f_full, ms_full)
+    peak_at = lambda mhz: n_cu * 4096 * mhz * 1e6 / 1e12 if mhz else None
+
+    def mode(f, key, mhz=None):
+        s_ = st[key]
+        d = {"ms": round(s_["mean"], 4), "median_ms": round(s_["median"], 4), "min_ms": round(s_["min"], 4),
+             "tflops": round(tfl(f, s_["mean"]), 2), "pct_peak": round(100 * tfl(f, s_["mean"]) / BF16_PEAK_TFLOPS, 2),
+             "flop": f}
+        if mhz:
+            d["sclk_mhz"] = round(mhz, 1)
+            d["pct_peak_at_measured_sclk"] = round(100 * tfl(f, s_["mean"]) / peak_at(mhz), 2)
+        return d
 
     out = {
         "metric": "joint-attn TFLOP/s (bf16, % MFMA peak) + attn-time speedup of adaptive reuse",
@@ -362,42 +436,33 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": "multi-reference image edit: batch 1, 24 heads, head_dim 128, 4096 target + "
-            "3x4096 reference-image + 256 text tokens (n_ref 12544); one block-step = Q-change, gate, "
-            "reuse attention (target queries, cached reference K/V), full-fresh attention (all queries), "
-            "cache commit",
-            "batch": B, "heads": H, "head_dim": D, "n_ref": n_ref, "n_tgt": n_tgt,
+            "3x4096 reference-image + 256 text tokens (n_ref 12544); one step = one denoising step of Alg. 1 "
+            "over three blocks on the device controller: each block runs the fused Q-change + gate, then "
+            "block 0 reuses (target queries over the cached reference K/V), block 1 is the reactivation "
+            "boundary (target queries and the cached reference queries over the cache) and block 2 computes "
+            "(all queries over fresh K/V) and commits its reference Q/K/V to the cache",
+            "batch": B, "heads": H, "head_dim": D, "n_ref": n_ref, "n_tgt": n_tgt, "blocks_per_step": NB,
         },
         "pct_bf16_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
         "modes": {
-            "reuse": {"ms": round(ms["reuse"], 4), "tflops": round(reuse_tflops, 2),
-                      "pct_peak": round(100 * reuse_tflops / BF16_PEAK_TFLOPS, 2), "flop": f_reuse},
-            "full_fresh": {"ms": round(ms["full"], 4), "tflops": round(full_tflops, 2),
-                           "pct_peak": round(100 * full_tflops / BF16_PEAK_TFLOPS, 2), "flop": f_full},
+            "reuse": mode(f_reuse, "b0_attn", sclk_reuse_mhz),
+            "reactivate": mode(f_full, "b1_attn"),
+            "full_fresh": mode(f_full, "b2_attn", sclk_mhz),
         },
-        "reuse_block_attn_speedup": round(ms["full"] / ms["reuse"], 3),
+        "phases_ms": {k: {kk: round(vv, 4) for kk, vv in v.items()} for k, v in st.items()},
+        "reuse_block_attn_speedup": round(ms_full / ms_reuse, 3),
+        "sclk_mhz": round(sclk_mhz, 1) if sclk_mhz else None,
+        "pct_peak_at_measured_sclk": round(100 * full_tflops / peak_at(sclk_mhz), 2) if sclk_mhz else None,
+        "compute_units": n_cu,
         "small_kernels": {
-            "q_change_gate_us": round(ms["qcg"] * 1e3, 2),
-            "q_change_gate_gbs": round((qc_bytes + B * H * n_tgt * 4) / (ms["qcg"] * 1e-3) / 1e9, 1),
-            "q_change_gate_hot_us": round(ms["qcg_hot"] * 1e3, 2),
-            "q_change_us": round(ms["qc"] * 1e3, 2),
-            "q_change_gbs": round(qc_bytes / (ms["qc"] * 1e-3) / 1e9, 1),
-            "q_change_hot_us": round(ms["qc_hot"] * 1e3, 2),
-            "gate_us": round(ms["gate"] * 1e3, 2),
-            "gate_gbs": round((B * H * n_tgt * 4 + B * H * 4) / (ms["gate"] * 1e-3) / 1e9, 1),
-            "gate_hot_us": round(ms["gate_hot"] * 1e3, 2),
-            "commit_us": round(ms["commit"] * 1e3, 2),
-            "commit_copy_us": round(ms["commit_copy"] * 1e3, 2),
-            "commit_copy_gbs": round(4 * B * H * n_ref * D * 2 / (ms["commit_copy"] * 1e-3) / 1e9, 1),
-            "diag_kv_drift_us": round(ms["kv_drift"] * 1e3, 2),
-            "diag_kv_drift_gbs": round(diag_bytes["kv_drift"] / (ms["kv_drift"] * 1e-3) / 1e9, 1),
-            "diag_drift_log_ratio_us": round(ms["ratio"] * 1e3, 2),
-            "diag_drift_log_ratio_gbs": round(diag_bytes["ratio"] / (ms["ratio"] * 1e-3) / 1e9, 1),
-            "diag_output_impact_us": round(ms["impact"] * 1e3, 2),
-            "diag_output_impact_gbs": round(diag_bytes["impact"] / (ms["impact"] * 1e-3) / 1e9, 1),
-            "diag_mass_mean_us": round(ms["mass_mean"] * 1e3, 2),
+            "commit_copy_us": round(st["b2_commit"]["mean"] * 1e3, 2),
+            "commit_copy_gbs": round(6 * B * H * n_ref * D * 2 / (st["b2_commit"]["mean"] * 1e-3) / 1e9, 1),
+            "commit_skip_us": round(st["b0_commit"]["mean"] * 1e3, 2),
+            **small,
         },
         "roofline": {
-            "kernel": "attn_bf16_kernel<128> (full-fresh mode, with the key-split merge of its last round)",
+            "kernel": "attn_bf16_kernel<128> (COMPUTE block: all queries over fresh K/V, with the key-split "
+                      "merge of its last round)",
             "bound": "mfma",
             "achieved": round(full_tflops, 2),
             "peak": BF16_PEAK_TFLOPS,
@@ -406,27 +471,36 @@ def main():
             "traffic": _traffic_from_profile(),
         },
     }
+    del ctl, set0
+    torch.cuda.empty_cache()
+
+    # ---- the metric's second half: one depth-adaptive controller trajectory against its
+    # full-fresh trajectory (60 blocks x 8 steps at the single-reference shapes)
+    from paper_2609_32415_amd.controller import adaptive_cell
+
+    out["adaptive_reuse"] = adaptive_cell(device=dev, log=log)
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         xs = {k: x1[k] for k in ("q_ref", "q_tgt", "k_ref", "v_ref", "k_tgt", "v_tgt")}
         out["cpu_baseline"] = cpu_baseline(xs, args.cpu_seconds)
     if args.sweep:
         from paper_2609_32415_amd.controller import run_sweep
 
-        out["sweep"] = run_sweep(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+        out["sweep"] = run_sweep(device=dev, log=log)
     if args.diagnostics:
         from paper_2609_32415_amd.controller import run_diagnostics
 
-        out["diagnostics"] = run_diagnostics(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+        out["diagnostics"] = run_diagnostics(device=dev, log=log)
     if args.segments:
         from paper_2609_32415_amd.controller import run_reference_segments
 
-        out["reference_segments"] = run_reference_segments(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+        out["reference_segments"] = run_reference_segments(device=dev, log=log)
     if args.shapes:
         out["shapes"] = time_shapes(dev)
     if args.ref_sweep:
         from paper_2609_32415_amd.controller import run_ref_count_sweep
 
-        out["ref_count_sweep"] = run_ref_count_sweep(device=dev, log=lambda m: print(m, file=sys.stderr, flush=True))
+        out["ref_count_sweep"] = run_ref_count_sweep(device=dev, log=log)
     print(json.dumps(out), flush=True)
 
 

@@ -119,6 +119,11 @@ typedef struct {
    * REACTIVATE under RA_KV_DEVICE (Alg. 1 boundary branch: the cached reference state is
    * restored and its queries attend to [cached K_R; current K_Y]). */
   ra_tensor q_cache;
+  /* Optional clock probe (bf16 path; ignored by fp32), or NULL: the first lane of every
+   * workgroup adds its shader-clock cycles to clock_probe[0] and the 100 MHz reference
+   * ticks over the same interval to clock_probe[1] (device uint64, added to, so the caller
+   * zeroes them). 100 MHz * [0] / [1] is the launch's mean shader clock. */
+  uint64_t* clock_probe;
 } ra_attn_args;
 
 /*

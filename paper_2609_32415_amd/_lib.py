@@ -102,6 +102,7 @@ class ra_attn_args(ctypes.Structure):
         ("seg_cache", ctypes.c_uint32),
         ("seg_mass", ctypes.c_void_p),
         ("q_cache", ra_tensor),
+        ("clock_probe", ctypes.c_void_p),
     ]
 
 

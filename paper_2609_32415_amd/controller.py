@@ -86,8 +86,12 @@ class Controller:
         self.attn_ws = ops.attn_workspace(q_like, n_ref, kvsrc="device")
         self.sidecar = sidecar
 
-    def block(self, t, b, x):
-        """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``."""
+    def block(self, t, b, x, mark=None, clock_probe=None):
+        """Enqueue Alg. 1's work for block ``b`` at step ``t`` on fresh inputs ``x``.
+
+        ``mark(name)`` (optional) is called after each enqueued phase ("gate", "attn",
+        "commit"), e.g. to record timing events; ``clock_probe`` is passed to the attention
+        launch (see ``ops.joint_attn``)."""
         if self.cue == "anchor":
             q_prev = self.q_anchor[b] if t > 0 else x["q_tgt"]
         else:
@@ -101,18 +105,25 @@ class Controller:
             ops.q_change(x["q_tgt"], q_prev, self.eps, out=self.d[b], workspace=self.ws)
             ops.gate(self.d[b], self.mass[b][self.parity[b]], self.theta, self.state, b, t, self.mode,
                      decision_out=dec, score_out=self.scores[t, b])
+        if mark:
+            mark("gate")
         nxt = 1 - self.parity[b]
         ops.joint_attn(
             x["q_tgt"], x["k_tgt"], x["v_tgt"], q_ref=x["q_ref"], k_ref=x["k_ref"], v_ref=x["v_ref"],
             k_cache=self.k_cache[b], v_cache=self.v_cache[b], q_cache=self.q_cache[b], kvsrc="device", decision=dec,
             o_tgt=self.o_tgt[b], o_ref=self.o_ref[b], ref_mass=self.mass[b][nxt], workspace=self.attn_ws,
+            clock_probe=clock_probe,
         )
+        if mark:
+            mark("attn")
         if self.sidecar is not None:  # read-only probes; the block's cache still holds its anchor K/V
             self.sidecar.block(t, b, x, self)
         ops.cache_commit(x["k_ref"], x["v_ref"], self.k_cache[b], self.v_cache[b], decision=dec,
                          age=self.age[b:b + 1], step=t, q_ref=x["q_ref"], q_cache=self.q_cache[b])
         if self.cue == "anchor":
             ops.cache_commit(x["q_tgt"], None, self.q_anchor[b], None, decision=dec)
+        if mark:
+            mark("commit")
         self.q_prev[b] = x["q_tgt"]
         self.parity[b] = nxt
 
@@ -320,6 +331,46 @@ def _cell(w, device, full_ms, theta, delta_max=None, mode="product", theta_m=Non
         "impact_p99": round(float(e.quantile(0.99)), 5),
         "impact_max": round(float(e.max()), 5),
     }
+
+
+def adaptive_cell(device="cuda:0", w=None, theta_q=0.2, theta_m=0.4, log=None):
+    """One depth-adaptive controller trajectory against its full-fresh trajectory.
+
+    The sweep workload (60 blocks x 8 steps at the single-reference shapes) runs once with a
+    refresh every step (every block computes: the full-fresh trajectory) and once under the
+    product gate at theta_q * theta_m, through the same harness. Reports the attention-path
+    times, the attention-time speedup of adaptive reuse, the reuse fractions over steps >= 1,
+    the reactivation boundary of every step and how many steps put it at each depth, the
+    relative change of the executed target output against full-fresh attention, and the
+    all-reuse bound of the speedup."""
+    w = w or synth.workload("sweep")
+    _, base_ms = _timed_run(w, device, 0.0, delta_max=1)
+    full_ms = sum(base_ms)
+    c = _cell(w, device, full_ms, theta_q * theta_m)
+    bnd = c["boundary_block_per_step"][1:]
+    hist = {}
+    for b in bnd:
+        key = "none" if b is None else str(b)
+        hist[key] = hist.get(key, 0) + 1
+    res = {
+        "workload": f"{w.n_blocks} blocks x {w.n_steps} steps, batch {w.batch}, {w.heads} heads, head_dim "
+                    f"{w.head_dim}, n_ref {w.n_ref}, n_tgt {w.n_tgt} (sweep recipe: exposure rising with depth, "
+                    f"target change decaying over the steps)",
+        "theta_q": theta_q, "theta_m": theta_m, "theta": theta_q * theta_m,
+        "full_fresh_attn_path_ms": round(full_ms, 3),
+        "adaptive_attn_path_ms": c["attn_path_ms"],
+        "attn_time_speedup": c["speedup_vs_full_fresh"],
+        "max_speedup_bound": round(w.n_steps / (1 + (w.n_steps - 1) * w.n_tgt / (w.n_ref + w.n_tgt)), 3),
+        "reuse_fraction": c["reuse_fraction"],
+        "reuse_or_reactivate_fraction": c["reuse_or_reactivate_fraction"],
+        "boundary_block_per_step": c["boundary_block_per_step"],
+        "boundary_depth_histogram": hist,
+        "impact_mean": c["impact_mean"], "impact_p99": c["impact_p99"], "impact_max": c["impact_max"],
+    }
+    if log:
+        log(f"adaptive reuse: {res['attn_time_speedup']}x over full-fresh ({res['full_fresh_attn_path_ms']} ms -> "
+            f"{res['adaptive_attn_path_ms']} ms), boundaries {res['boundary_block_per_step']}")
+    return res
 
 
 def _graph_timed_run(w, device, theta, delta_max):

@@ -263,6 +263,7 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   p.lse_tgt = a.lse_tgt;
   p.mass_refq = a.ref_mass_refq;
   p.decision = a.decision;
+  p.clock_probe = reinterpret_cast<unsigned long long*>(a.clock_probe);
   p.B = d.batch;
   p.H = d.heads;
   p.n_ref = d.n_ref;

@@ -240,6 +240,21 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const int nt = n_rt + n_yt;
   const int w = blockIdx.x;
   if (w >= pl.total_items) return;
+  // Optional clock probe: shader-clock cycles and 100 MHz reference ticks over this
+  // workgroup's life, added to the caller's counters by its first lane at exit.
+  const bool probe = p.clock_probe != nullptr;
+  uint64_t clk0 = 0, rt0 = 0;
+  if (probe) {
+    clk0 = __builtin_amdgcn_s_memtime();
+    rt0 = __builtin_amdgcn_s_memrealtime();
+  }
+  auto probe_end = [&]() {
+    if (probe && tid == 0) {
+      const uint64_t clk1 = __builtin_amdgcn_s_memtime(), rt1 = __builtin_amdgcn_s_memrealtime();
+      atomicAdd(p.clock_probe, (unsigned long long)(clk1 - clk0));
+      atomicAdd(p.clock_probe + 1, (unsigned long long)(rt1 - rt0));
+    }
+  };
   int tile, j0 = 0, j1 = nt, slot = -1;
   if (w < pl.whole) {
     tile = xcd_remap(w, pl.whole);
@@ -603,6 +618,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
               float4{o[db][4 * rr], o[db][4 * rr + 1], o[db][4 * rr + 2], o[db][4 * rr + 3]};
       if (g == 0) p.part_st[prow] = float4{m_run, l_run, m_ref, l_ref};
     }
+    probe_end();
     return;
   }
 
@@ -644,6 +660,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       }
     }
   }
+  probe_end();
 }
 
 // Combines the key chunks of split query tiles: one row per D/4 threads, four

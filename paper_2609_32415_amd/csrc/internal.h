@@ -40,6 +40,7 @@ struct AttnParams {
   float* lse_tgt;           // [B, H, n_tgt, 2] or null
   float* mass_refq;         // [B, H, n_ref] or null
   const int32_t* decision;  // KV_DEVICE only
+  unsigned long long* clock_probe;  // [2] shader cycles, 100 MHz ticks (added to), or null
   int32_t B, H, n_ref, n_tgt;
   int32_t qt_ref;       // query tiles per (b, h) over reference rows (0 when they do not attend)
   int32_t qt_tgt;       // query tiles per (b, h) over target rows

@@ -56,6 +56,13 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _probe_ptr(t):
+    _on_gpu("clock_probe", t)
+    if t.dtype != torch.int64 or t.numel() != 2 or not t.is_contiguous():
+        raise ValueError("clock_probe must be a contiguous int64 device tensor of 2 elements")
+    return t.data_ptr()
+
+
 @dataclass
 class AttnOut:
     o_tgt: torch.Tensor
@@ -91,6 +98,7 @@ def joint_attn(
     seg_end=None,
     seg_cache=None,
     seg_mass=False,
+    clock_probe=None,
 ):
     """Joint attention over [K_R; K_Y] through ``refadapt_joint_attn``.
 
@@ -99,6 +107,10 @@ def joint_attn(
     workspace the library asks for (torch caching allocator), False runs
     without key splits, a uint8 device tensor is used as given (see
     ``attn_workspace``). Returns an ``AttnOut``.
+
+    ``clock_probe``: an int64 device tensor of 2 elements that the bf16 kernel adds its
+    workgroups' shader-clock cycles and 100 MHz reference ticks to (mean clock = 100 MHz x
+    [0] / [1]); None disables it.
 
     ``q_cache``: reference queries of the cached state; reference queries that attend
     over the cached K/V (``kvsrc="cache"`` with ``qset="all"``, or REACTIVATE under
@@ -184,6 +196,7 @@ def joint_attn(
         seg_cache=cache_bits,
         seg_mass=None if smass_t is None else smass_t.data_ptr(),
         q_cache=_view("q_cache", q_cache, dt, shp_r),
+        clock_probe=None if clock_probe is None else _probe_ptr(clock_probe),
     )
     L.refadapt_joint_attn(desc, args, _stream())
     return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t, smass_t)

@@ -574,3 +574,21 @@ def test_random_configurations_parity(case):
         rr = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
         assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]
         assert max_abs(host(got.ref_mass_refq), rr["ref_mass"]) <= MASS_TOL["bf16"]
+
+
+def test_clock_probe_counts_and_leaves_outputs_unchanged():
+    """The optional clock probe adds every workgroup's shader cycles and 100 MHz ticks; the
+    outputs are bitwise those of the launch without it."""
+    print("clock probe", flush=True)
+    _, x = _inputs("bf16", 128, 700, 900, 1, 4)
+    plain = _gpu(x, "bf16", "all", "fresh")
+    probe = torch.zeros(2, dtype=torch.int64, device="cuda:0")
+    got = _gpu(x, "bf16", "all", "fresh", clock_probe=probe)
+    for a, b in ((plain.o_tgt, got.o_tgt), (plain.o_ref, got.o_ref), (plain.ref_mass, got.ref_mass),
+                 (plain.lse, got.lse)):
+        assert torch.equal(a, b)
+    cyc, ticks = probe.cpu().tolist()
+    assert ticks > 0 and cyc > 0
+    mhz = 100.0 * cyc / ticks
+    print(f"  mean shader clock {mhz:.0f} MHz", flush=True)
+    assert 300.0 < mhz < 3000.0
