@@ -49,32 +49,49 @@ __global__ __launch_bounds__(QC_THREADS) void pair_partial(PairSet ps, int32_t H
   if (threadIdx.x == 0) ws[((int64_t)pair * gridDim.y + bh) * chunks_max + blockIdx.x] = v;
 }
 
-__device__ __forceinline__ double pair_ratio(const float2* ws, int pair, int bh, int bh_total, int chunks,
-                                             int chunks_max, double eps) {
-  double a = 0.0, c = 0.0;
-  for (int i = 0; i < chunks; ++i) {
-    const float2 v = ws[((int64_t)pair * bh_total + bh) * chunks_max + i];
-    a += v.x;
-    c += v.y;
-  }
-  return sqrt(a) / (sqrt(c) + eps);
-}
+// Pass 2: a workgroup takes PF_HEADS (b, h) pairs, stages each pair's chunk partials in LDS
+// (one coalesced memory round trip), and one thread per (b, h) adds them in chunk order in
+// fp64 and combines the pairs.
+constexpr int PF_THREADS = 256;
+constexpr int PF_HEADS = 32;
 
-// Pass 2: per (b, h), add each pair's chunk partials in order and combine.
-__global__ __launch_bounds__(256) void pair_final(const float2* ws, PairSet ps, int32_t bh_total, int32_t chunks_max,
-                                                  int32_t kind, float eps, float* out0, float* out1, float* out2) {
-  const int bh = blockIdx.x * blockDim.x + threadIdx.x;
-  if (bh >= bh_total) return;
+__global__ __launch_bounds__(PF_THREADS) void pair_final(const float2* ws, PairSet ps, int32_t bh_total,
+                                                         int32_t chunks_max, int32_t kind, float eps, float* out0,
+                                                         float* out1, float* out2) {
+  __shared__ float2 s_part[2][PF_HEADS * (QC_MAX_CHUNKS + 1)];
+  const int h0 = blockIdx.x * PF_HEADS;
+  const int nh = min(PF_HEADS, bh_total - h0);
+  const int npairs = kind == PAIR_SINGLE ? 1 : 2;
+  for (int pr = 0; pr < npairs; ++pr) {
+    // pair pr's records of (b, h) lie at ws[(pr * bh_total + bh) * chunks_max + c], c < chunks
+    const float2* src = ws + ((int64_t)pr * bh_total + h0) * chunks_max;
+    const int n = nh * chunks_max;
+    for (int i = threadIdx.x; i < n; i += PF_THREADS) {
+      const int hh = i / chunks_max, c = i - hh * chunks_max;
+      if (c < ps.chunks[pr]) s_part[pr][hh * (chunks_max + 1) + c] = src[i];
+    }
+  }
+  __syncthreads();
+  if ((int)threadIdx.x >= nh) return;
+  const int bh = h0 + threadIdx.x;
   const double e = (double)eps;
-  const double d0 = pair_ratio(ws, 0, bh, bh_total, ps.chunks[0], chunks_max, e);
+  double d[2] = {0.0, 0.0};
+  for (int pr = 0; pr < npairs; ++pr) {
+    const float2* r = s_part[pr] + threadIdx.x * (chunks_max + 1);
+    double a = 0.0, c = 0.0;
+    for (int i = 0; i < ps.chunks[pr]; ++i) {
+      a += r[i].x;
+      c += r[i].y;
+    }
+    d[pr] = sqrt(a) / (sqrt(c) + e);
+  }
   if (kind == PAIR_SINGLE) {
-    out0[bh] = (float)d0;
+    out0[bh] = (float)d[0];
     return;
   }
-  const double d1 = pair_ratio(ws, 1, bh, bh_total, ps.chunks[1], chunks_max, e);
-  if (out0) out0[bh] = (float)d0;
-  if (out1) out1[bh] = (float)d1;
-  out2[bh] = (float)(kind == PAIR_KV ? 0.5 * (d0 + d1) : log10((d0 + e) / (d1 + e)));
+  if (out0) out0[bh] = (float)d[0];
+  if (out1) out1[bh] = (float)d[1];
+  out2[bh] = (float)(kind == PAIR_KV ? 0.5 * (d[0] + d[1]) : log10((d[0] + e) / (d[1] + e)));
 }
 
 // One workgroup per (b, h): mean of mass (or 1 - mass) over n rows.
@@ -145,8 +162,8 @@ hipError_t launch_pair_change(int dtype, int32_t B, int32_t H, int32_t head_dim,
                  : launch_kernel(pair_partial<false>, grid, dim3(QC_THREADS), 0, stream, ps, H, head_dim, cmax, w);
   if (e != hipSuccess) return e;
   const int bh = B * H;
-  return launch_kernel(pair_final, dim3((bh + 255) / 256), dim3(256), 0, stream, w, ps, bh, cmax, kind, eps, out0,
-                       out1, out2);
+  return launch_kernel(pair_final, dim3((bh + PF_HEADS - 1) / PF_HEADS), dim3(PF_THREADS), 0, stream, w, ps, bh,
+                       cmax, kind, eps, out0, out1, out2);
 }
 
 hipError_t launch_mass_mean(int32_t B, int32_t H, int32_t n, const float* mass, int complement, float* out,

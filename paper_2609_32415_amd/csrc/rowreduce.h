@@ -17,7 +17,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int QC_THREADS = 256;
 constexpr int QC_TARGET_ELEMS = 16384;  // elements of one tensor per workgroup (32 KiB of bf16)
 constexpr int QC_MAX_CHUNKS = 64;
-constexpr int QC_UNROLL = 4;  // 16-byte vectors of each tensor per thread in flight
+constexpr int QC_UNROLL = 8;  // 16-byte vectors of each tensor per thread in flight
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -27,6 +27,19 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
   return v;
+}
+
+// Stages the chunk partials of heads [h0, h0 + nh) (`chunks` records of T per head, head
+// major) in LDS with coalesced loads by the whole workgroup, head i at s[i * (chunks + 1)]
+// (the padding spreads the per-head rows over the banks). One memory round trip.
+template <typename T>
+__device__ __forceinline__ void stage_partials(T* s, const T* part, int h0, int nh, int chunks) {
+  const int n = nh * chunks;
+  const T* src = part + (int64_t)h0 * chunks;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int hh = i / chunks, c = i - hh * chunks;
+    s[hh * (chunks + 1) + c] = src[i];
+  }
 }
 
 // Sums (cur - prev)^2 and prev^2 over rows [r0, r1) of one (b, h), returned to thread 0

@@ -29,18 +29,26 @@ __global__ __launch_bounds__(QC_THREADS) void q_change_partial(View cur, View pr
   if (threadIdx.x == 0) ws[(int64_t)bh * chunks + blockIdx.x] = v;
 }
 
-// Pass 2: per (b, h), add the chunk partials in order (fp64) and form D.
-__global__ __launch_bounds__(256) void q_change_final(const float2* ws, int32_t bh_total, int32_t chunks, float eps,
-                                                      float* out) {
-  const int bh = blockIdx.x * blockDim.x + threadIdx.x;
-  if (bh >= bh_total) return;
+// Pass 2: a workgroup takes QF_HEADS (b, h) pairs, stages their chunk partials in LDS (one
+// coalesced memory round trip), and one thread per pair adds them in chunk order in fp64.
+constexpr int QF_THREADS = 256;
+constexpr int QF_HEADS = 64;
+
+__global__ __launch_bounds__(QF_THREADS) void q_change_final(const float2* ws, int32_t bh_total, int32_t chunks,
+                                                             float eps, float* out) {
+  __shared__ float2 s_part[QF_HEADS * (QC_MAX_CHUNKS + 1)];
+  const int h0 = blockIdx.x * QF_HEADS;
+  const int nh = min(QF_HEADS, bh_total - h0);
+  stage_partials(s_part, ws, h0, nh, chunks);
+  __syncthreads();
+  if ((int)threadIdx.x >= nh) return;
+  const float2* r = s_part + threadIdx.x * (chunks + 1);
   double a = 0.0, c = 0.0;
   for (int i = 0; i < chunks; ++i) {
-    const float2 v = ws[(int64_t)bh * chunks + i];
-    a += v.x;
-    c += v.y;
+    a += r[i].x;
+    c += r[i].y;
   }
-  out[bh] = (float)(sqrt(a) / (sqrt(c) + (double)eps));
+  out[h0 + threadIdx.x] = (float)(sqrt(a) / (sqrt(c) + (double)eps));
 }
 
 // Alg. 1 block branch on one thread: step bookkeeping at block 0 (step 0, or step -
@@ -114,7 +122,7 @@ __global__ __launch_bounds__(GATE_THREADS) void gate_kernel(int32_t BH, int32_t 
                                                             float* score_out) {
   extern __shared__ float s_dm[];  // [2 * BH]: D (copied from d_cur), then the mean lagged mass
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  GateInputs gin;
+  GateInputs gin{};
   if (tid == 0) gin = gate_load(st, theta, block, mode);
   for (int i = tid; i < BH; i += GATE_THREADS) s_dm[i] = d_cur[i];
 
@@ -168,10 +176,21 @@ __global__ __launch_bounds__(QC_THREADS) void q_change_mass_partial(View cur, Vi
   const int bh = blockIdx.y;
   const int b = bh / H, h = bh - b * H;
   const int2 rr = chunk_rows(n_rows, chunks);
-  const float2 v = q_change_rows<BF16>(cur, prev, b, h, rr.x, rr.y, head_dim);
+  // The first MP lagged-mass values of this thread's rows are loaded before the Q-change
+  // loads, so both share one memory round trip; the per-thread order is the strided one.
+  constexpr int MP = 4;
   const float* mrow = mass_prev + (int64_t)bh * n_rows;
+  float mv[MP];
+#pragma unroll
+  for (int k = 0; k < MP; ++k) {
+    const int i = rr.x + threadIdx.x + k * QC_THREADS;
+    mv[k] = i < rr.y ? mrow[i] : 0.f;
+  }
+  const float2 v = q_change_rows<BF16>(cur, prev, b, h, rr.x, rr.y, head_dim);
   float sm = 0.f;
-  for (int i = rr.x + threadIdx.x; i < rr.y; i += QC_THREADS) sm += mrow[i];
+#pragma unroll
+  for (int k = 0; k < MP; ++k) sm += mv[k];
+  for (int i = rr.x + threadIdx.x + MP * QC_THREADS; i < rr.y; i += QC_THREADS) sm += mrow[i];
   sm = wave_sum(sm);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = sm;
   __syncthreads();
@@ -184,29 +203,43 @@ __global__ __launch_bounds__(QC_THREADS) void q_change_mass_partial(View cur, Vi
 }
 
 constexpr int QG_THREADS = 256;
+constexpr int QG_STAGE = 1024;  // float4 partial records staged in LDS per round (16 KiB)
 
+// Pass 2 of the fused Q-change + gate (one workgroup): rounds of (b, h) pairs have their
+// chunk partials staged in LDS (one coalesced memory round trip per round, a single round
+// up to 1024 / chunks pairs); one thread per pair adds them in chunk order in fp64 and
+// writes D and the mean lagged mass; then thread 0 decides.
 __global__ __launch_bounds__(QG_THREADS) void q_change_gate_final(const float4* part, int32_t BH, int32_t chunks,
                                                                   int32_t n_rows, float eps, int32_t block,
                                                                   int32_t step, int32_t mode, const float* theta,
                                                                   GateState* st, float* d_out, int32_t* decision_out,
                                                                   float* score_out) {
   extern __shared__ float s_dm[];  // [2 * BH]: D, then the mean lagged mass of each (b, h)
-  GateInputs gin;
+  // a round holds nh <= QG_STAGE / chunks pairs (at most QG_THREADS) of chunks + 1 records
+  __shared__ float4 s_part[QG_STAGE + QG_THREADS];
+  GateInputs gin{};
   if (threadIdx.x == 0) gin = gate_load(st, theta, block, mode);
-  for (int i = threadIdx.x; i < BH; i += QG_THREADS) {
-    double a = 0.0, c = 0.0, ms = 0.0;
-    for (int k = 0; k < chunks; ++k) {
-      const float4 pk = part[(int64_t)i * chunks + k];
-      a += pk.x;
-      c += pk.y;
-      ms += pk.z;
+  const int per_round = max(1, min(QG_THREADS, QG_STAGE / chunks));
+  for (int h0 = 0; h0 < BH; h0 += per_round) {
+    const int nh = min(per_round, BH - h0);
+    stage_partials(s_part, part, h0, nh, chunks);
+    __syncthreads();
+    if ((int)threadIdx.x < nh) {
+      const float4* r = s_part + threadIdx.x * (chunks + 1);
+      double a = 0.0, c = 0.0, ms = 0.0;
+      for (int k = 0; k < chunks; ++k) {
+        a += r[k].x;
+        c += r[k].y;
+        ms += r[k].z;
+      }
+      const int i = h0 + threadIdx.x;
+      const float dv = (float)(sqrt(a) / (sqrt(c) + (double)eps));
+      d_out[i] = dv;
+      s_dm[i] = dv;
+      s_dm[BH + i] = (float)(ms / n_rows);
     }
-    const float dv = (float)(sqrt(a) / (sqrt(c) + (double)eps));
-    d_out[i] = dv;
-    s_dm[i] = dv;
-    s_dm[BH + i] = (float)(ms / n_rows);
+    __syncthreads();
   }
-  __syncthreads();
   if (threadIdx.x == 0) gate_decide(BH, block, step, mode, s_dm, s_dm + BH, gin, st, decision_out, score_out);
 }
 
@@ -258,7 +291,8 @@ hipError_t launch_q_change(int dtype, int32_t B, int32_t H, int32_t n_tgt, int32
                           chunks, w);
   if (e != hipSuccess) return e;
   const int bh = B * H;
-  return launch_kernel(q_change_final, dim3((bh + 255) / 256), dim3(256), 0, stream, w, bh, chunks, eps, d_out);
+  return launch_kernel(q_change_final, dim3((bh + QF_HEADS - 1) / QF_HEADS), dim3(QF_THREADS), 0, stream, w, bh,
+                       chunks, eps, d_out);
 }
 
 hipError_t launch_gate(int32_t B, int32_t H, int32_t n_tgt, int32_t block, int32_t step, int32_t mode,
