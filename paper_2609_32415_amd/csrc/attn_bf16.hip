@@ -382,17 +382,46 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   // cursors of the in-loop loads: K from tile j0 + 2, V from tile j0 + 1
   DmaCursor<D, true> kc;
   DmaCursor<D, false> vc;
-  auto cursor_view = [&](auto& cur, bool is_k, int tile) {
-    if (tile < n_rt)
-      cur.set_view(is_k ? kr : vr, is_k ? kr_ss : vr_ss, is_k ? voff_r : voff_rv, tile, tile * BN, p.n_ref, wave_u);
-    else
-      cur.set_view(is_k ? ky : vy, is_k ? ky_ss : vy_ss, is_k ? voff_yk : voff_yv, tile, (tile - n_rt) * BN, p.n_tgt,
+  // SEG: the segment each cursor reads and the key tile that ends it. A cursor re-targets to
+  // the next segment's base (this (b, h) applied) when it reaches that tile; segments share
+  // the reference views' strides, so only the base pointer changes. The segment tables are
+  // read through pointers into the kernel arguments (indexing the by-value copy at run time
+  // would place it in scratch memory).
+  int kc_seg = 0, kc_end = 0, vc_seg = 0, vc_end = 0;
+  const int32_t* const seg_end_tab = p.seg_tile_end;
+  const void* const* const seg_k_tab = p.seg_kbase;
+  const void* const* const seg_v_tab = p.seg_vbase;
+  auto cursor_view = [&](auto is_kc, auto& cur, int tile) __attribute__((always_inline)) {
+    constexpr bool IS_K = decltype(is_kc)::value;
+    if (tile < n_rt) {
+      const uint16_t* base = IS_K ? kr : vr;
+      if constexpr (SEG) {
+        int sg = 0;
+        while (tile >= seg_end_tab[sg] && sg + 1 < p.n_seg) ++sg;
+        base = static_cast<const uint16_t*>((IS_K ? seg_k_tab : seg_v_tab)[sg]) + (IS_K ? kbh : vbh);
+        (IS_K ? kc_seg : vc_seg) = sg;
+        (IS_K ? kc_end : vc_end) = seg_end_tab[sg];
+      }
+      cur.set_view(base, IS_K ? kr_ss : vr_ss, IS_K ? voff_r : voff_rv, tile, tile * BN, p.n_ref, wave_u);
+    } else {
+      cur.set_view(IS_K ? ky : vy, IS_K ? ky_ss : vy_ss, IS_K ? voff_yk : voff_yv, tile, (tile - n_rt) * BN, p.n_tgt,
                    wave_u);
+    }
   };
-  if constexpr (!SEG) {
-    cursor_view(kc, true, j0 + 2);
-    cursor_view(vc, false, j0 + 1);
-  }
+  // SEG: moves a cursor that reached its segment's last tile to the next segment (same rows,
+  // same strides: the row pointer moves by the difference of the two segments' bases).
+  auto cursor_next_seg = [&](auto is_kc, auto& cur) __attribute__((always_inline)) {
+    constexpr bool IS_K = decltype(is_kc)::value;
+    int& sg = IS_K ? kc_seg : vc_seg;
+    const void* const* tab = IS_K ? seg_k_tab : seg_v_tab;
+    const char* from = static_cast<const char*>(tab[sg]);
+    ++sg;
+    (IS_K ? kc_end : vc_end) = seg_end_tab[sg];
+    cur.ptr = reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(cur.ptr) +
+                                                (static_cast<const char*>(tab[sg]) - from));
+  };
+  cursor_view(std::true_type{}, kc, j0 + 2);
+  cursor_view(std::false_type{}, vc, j0 + 1);
 
   f32x16 o[DB];
 #pragma unroll
@@ -407,16 +436,9 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   // jbc: the LDS buffer of K_j and V_j, (j - j0) & 1, as a compile-time constant.
   auto iteration = [&](auto jbc, int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
     constexpr int jb = decltype(jbc)::value;
-    // Segment kernel: keep the per-workgroup tile sources in registers (rematerialising them
-    // from the kernel arguments would put a scalar load under the first MFMA's LDS wait). The
-    // other kernels address their loads through the K and V cursors instead.
-    if constexpr (SEG) {
-      asm volatile("" : "+s"(kr), "+s"(vr), "+s"(ky), "+s"(vy));
-      asm volatile("" : "+s"(kr_ss), "+s"(vr_ss), "+s"(ky_ss), "+s"(vy_ss));
-    }
     // Global loads for the tiles this iteration stages: K_{j+2} and V_{j+1}, issued at the
-    // start of phase B. Past the workgroup's last key tile the segment kernel reloads that
-    // tile into a buffer that is never read again; the cursors skip the load.
+    // start of phase B through the K and V cursors; past the workgroup's last key tile the
+    // cursors skip the load.
     uint16_t* const kb_cur = jb ? kbuf1 : kbuf0;   // K_j (already read), refilled with K_{j+2}
     uint16_t* const kb_next = jb ? kbuf0 : kbuf1;  // K_{j+1}
     uint16_t* const vb_cur = jb ? vbuf1 : vbuf0;   // V_j
@@ -517,18 +539,21 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     if (partner) __builtin_amdgcn_s_setprio(0); else __builtin_amdgcn_s_setprio(1);
     // The next tiles' direct loads: issued here rather than at the top of the iteration, so
     // their LDS writes do not land under phase A's K operand reads (about -1.5%).
-    if constexpr (SEG) {
-      load_k(kb_cur, min(j + 2, j1 - 1));
-      load_v(vb_next, min(j + 1, j1 - 1));
-    } else {
-      if (kc.t < j1) {
-        if (kc.t == n_rt) cursor_view(kc, true, kc.t);
-        kc.load(kb_cur, wave_u);
+    if (kc.t < j1) {
+      if (kc.t == n_rt) {
+        cursor_view(std::true_type{}, kc, kc.t);
+      } else if constexpr (SEG) {
+        if (kc.t == kc_end) cursor_next_seg(std::true_type{}, kc);
       }
-      if (vc.t < j1) {
-        if (vc.t == n_rt) cursor_view(vc, false, vc.t);
-        vc.load(vb_next, wave_u);
+      kc.load(kb_cur, wave_u);
+    }
+    if (vc.t < j1) {
+      if (vc.t == n_rt) {
+        cursor_view(std::false_type{}, vc, vc.t);
+      } else if constexpr (SEG) {
+        if (vc.t == vc_end) cursor_next_seg(std::false_type{}, vc);
       }
+      vc.load(vb_next, wave_u);
     }
     const uint16_t* vs = vb_cur;
     auto v_operand = [&](int i) {  // i = DB * s2 + db
@@ -765,6 +790,13 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
     }
   }
 }
+
+// Explicit instantiations: without them the host pass leaves the segment instances, which
+// are only reached through the launcher's kernel-pointer argument, without launch stubs.
+template __global__ void attn_bf16_kernel<128, false>(AttnParams);
+template __global__ void attn_bf16_kernel<64, false>(AttnParams);
+template __global__ void attn_bf16_kernel<128, true>(AttnParams);
+template __global__ void attn_bf16_kernel<64, true>(AttnParams);
 
 }  // namespace
 
