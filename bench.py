@@ -64,6 +64,8 @@ def parse_args():
     # milliseconds of load to come back up
     ap.add_argument("--warmup", type=int, default=15)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-adaptive", action="store_true",
+                    help="skip the depth-adaptive controller trajectory (e.g. for short counter passes)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target duration of the oracle sample")
     ap.add_argument("--sweep", action="store_true", help="also run the 60-block x 8-step controller sweep")
     ap.add_argument("--diagnostics", action="store_true",
@@ -476,10 +478,11 @@ def main():
 
     # ---- the metric's second half: one depth-adaptive controller trajectory against its
     # full-fresh trajectory (60 blocks x 8 steps at the single-reference shapes)
-    from paper_2609_32415_amd.controller import adaptive_cell
+    if not args.no_adaptive:
+        from paper_2609_32415_amd.controller import adaptive_cell
 
-    out["adaptive_reuse"] = adaptive_cell(device=dev, log=log)
-    torch.cuda.empty_cache()
+        out["adaptive_reuse"] = adaptive_cell(device=dev, log=log)
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         xs = {k: x1[k] for k in ("q_ref", "q_tgt", "k_ref", "v_ref", "k_tgt", "v_tgt")}
         out["cpu_baseline"] = cpu_baseline(xs, args.cpu_seconds)
