@@ -13,10 +13,12 @@
 // row-major V tile with ds_read_b64_tr_b16 (LDS transpose read).
 //
 // Software pipeline (per wavefront): iteration j issues the 16 MFMAs of S_{j+1}
-// each followed by one pair of probabilities of S_j (phase A: pairs 0..9), then
-// the 16 MFMAs of O += V_j^T P_j^T, under the first six of which the remaining
-// pairs 10..15 are formed (phase B). sched_barrier fences keep that
-// order, so the vector ALU works while the matrix core runs. K tiles run one
+// with the probabilities of S_j pairs 0..9 formed under them (phase A), then
+// the 16 MFMAs of O += V_j^T P_j^T, under the first eight of which the remaining
+// pairs 10..15 are formed (phase B). A pair takes three MFMA slots (exponent
+// arguments, exponentials, row-sum adds and bf16 pack), so the instructions of
+// one slot never wait on each other. sched_barrier fences keep that order, so
+// the vector ALU works while the matrix core runs. K tiles run one
 // tile ahead of V tiles through two LDS buffers each. At the start of phase B of
 // iteration j direct global-to-LDS loads (no staging registers, no LDS store
 // instructions) fill the buffers that held K_j and V_{j-1} with K_{j+2} and
@@ -488,6 +490,42 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       pin(w);
       pw[q >> 2][q & 3] = w;
     };
+    // Software pipeline of the pairs over the MFMA slots: a slot forms the exponent
+    // arguments of pair k, the exponentials of pair k - 1 and the row-sum adds and bf16 pack
+    // of pair k - 2, so no instruction of a slot waits on another of the same slot.
+    float pa0 = 0.f, pa1 = 0.f;  // exponent arguments of the pair started one slot earlier
+    float pe0 = 0.f, pe1 = 0.f;  // exponentials of the pair started two slots earlier
+    auto pair_fin = [&](int q) {
+      if (q < 8) {
+        rs_a += pe0 + pe1;
+        pin(rs_a);
+      } else {
+        rs_b += pe0 + pe1;
+        pin(rs_b);
+      }
+      bf16x2 pr;
+      pr[0] = (__bf16)pe0;
+      pr[1] = (__bf16)pe1;
+      uint32_t w = __builtin_bit_cast(uint32_t, pr);
+      pin(w);
+      pw[q >> 2][q & 3] = w;
+    };
+    auto pipe_slot = [&](int k, int lo, int hi) {  // pairs lo..hi-1
+      if (k - 2 >= lo && k - 2 < hi) pair_fin(k - 2);
+      if (k - 1 >= lo && k - 1 < hi) {
+        pe0 = __builtin_amdgcn_exp2f(pa0);
+        pe1 = __builtin_amdgcn_exp2f(pa1);
+        pin(pe0);
+        pin(pe1);
+      }
+      if (k >= lo && k < hi) {
+        const int mb = k >> 3, o2 = (2 * k) & 15;
+        pa0 = fmaf(s_cur[mb][o2], c, -m_new);
+        pa1 = fmaf(s_cur[mb][o2 + 1], c, -m_new);
+        pin(pa0);
+        pin(pa1);
+      }
+    };
     // Row max of the lane's scores in key blocks mb0..1, shared by the lane pair of a query.
     auto tile_max = [&](int mb0) {
       float m = s_cur[1][0];
@@ -512,13 +550,11 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     for (int i = 0; i < NQK; ++i) {
       s_next[i / KS] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i & 3], qreg[i % KS], s_next[i / KS], 0, 0, 0);
       if (i + 4 < NQK) ka[i & 3] = k_operand(i + 4);
-      if (i < 10) prob_pair(i);  // P blocks 0, 1 and half of block 2
+      if (i < 12) pipe_slot(i, 0, 10);  // pairs 0..9: P blocks 0, 1 and half of block 2
       __builtin_amdgcn_sched_barrier(0);
     }
-    if (NQK < 10) {  // head_dim 64: fewer MFMAs than slices
 #pragma unroll
-      for (int q = NQK; q < 10; ++q) prob_pair(q);
-    }
+    for (int k = NQK; k < 12; ++k) pipe_slot(k, 0, 10);  // head_dim 64: fewer MFMAs than slots
     if (__any(!(rs_a + rs_b <= PBOUND))) {
       // Rare (always at a workgroup's first tile): move the max to the tile's row max
       // (nothing of this tile is in O^T yet) and form pairs 0..9 again.
@@ -574,7 +610,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
           __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[i % 3], __builtin_bit_cast(bf16x8, pwv), o[i % DB], 0, 0, 0);
       if (i + 2 < NPV) va[(i + 2) % 3] = v_operand(i + 2);
       // pairs 10..15 complete P blocks 2 and 3 before the first MFMA that reads them
-      if (DB == 4 && i < 6) prob_pair(10 + i);
+      if (DB == 4 && i < 8) pipe_slot(10 + i, 10, 16);
       if (DB == 2 && i < 3) {
         prob_pair(10 + 2 * i);
         prob_pair(11 + 2 * i);
