@@ -257,18 +257,19 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       atomicAdd(p.clock_probe + 1, (unsigned long long)(rt1 - rt0));
     }
   };
+  const int qt_bh = qt_ref + p.qt_tgt;
   int tile, j0 = 0, j1 = nt, slot = -1;
   if (w < pl.whole) {
-    tile = xcd_remap(w, pl.whole);
+    tile = plan_whole_tile(xcd_remap(w, pl.whole), qt_bh, p.B * p.H, pl.split_tiles);
   } else {  // key chunk c of a split tile: key tiles [c * nt / chunks, (c + 1) * nt / chunks)
-    // The chunks of neighbouring tiles of one (batch, head) go to one XCD, as whole tiles do.
+    // The chunks of neighbouring split tiles go to one XCD, as whole tiles do; both
+    // enumerations go head by head, so an XCD's chunks belong to its whole tiles' heads.
     slot = xcd_remap(w - pl.whole, pl.total_items - pl.whole);
     const int st = slot / pl.chunks, c = slot - st * pl.chunks;
-    tile = pl.whole + st;
+    tile = plan_split_tile(st, qt_bh, p.B * p.H, pl.split_tiles);
     j0 = c * nt / pl.chunks;
     j1 = (c + 1) * nt / pl.chunks;
   }
-  const int qt_bh = qt_ref + p.qt_tgt;
   const int bh = tile / qt_bh;
   int qt = tile - bh * qt_bh;
   const int b = bh / p.H, h = bh - b * p.H;
@@ -743,8 +744,8 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const int r = blockIdx.x * RPB + threadIdx.x / TPR, col = 4 * (threadIdx.x % TPR);
   const int st = r / BM, rr = r - st * BM;
   if (st >= pl.split_tiles) return;
-  const int tile = pl.whole + st;
   const int qt_bh = qt_ref + p.qt_tgt;
+  const int tile = plan_split_tile(st, qt_bh, p.B * p.H, pl.split_tiles);
   const int bh = tile / qt_bh;
   int qt = tile - bh * qt_bh;
   const bool ref_rows = qt < qt_ref;

@@ -21,9 +21,10 @@ enum { DEC_REUSE = 0, DEC_REACTIVATE = 1, DEC_COMPUTE = 2 };
 
 // Work decomposition of one bf16 attention launch over its query tiles (all
 // tiles of a (batch, head) attend to every key tile, so they cost the same).
-// Launch indices [0, whole) run whole query tiles; the last `split_tiles`
-// query tiles are cut into `chunks` contiguous key-tile ranges each, launched
-// at [whole, total_items), whose partial results a merge kernel combines.
+// Launch indices [0, whole) run whole query tiles; `split_tiles` query tiles
+// (the last ones of each (batch, head), plan_split_tile) are cut into `chunks`
+// contiguous key-tile ranges each, launched at [whole, total_items), whose
+// partial results a merge kernel combines.
 struct SplitPlan {
   int32_t whole;        // query tiles run whole (a multiple of the resident workgroup slots)
   int32_t split_tiles;  // query tiles run in key chunks
@@ -151,6 +152,48 @@ __device__ __forceinline__ int xcd_remap(int w, int total) {
   const int per = total >> 3, rem = total & 7;
   const int xcd = w & 7, k = w >> 3;
   return xcd * per + (xcd < rem ? xcd : rem) + k;
+}
+
+// Query tiles in the order a split plan enumerates them. The plan's split tiles
+// are spread evenly over the n_bh (batch, head) pairs, the last ones of each
+// (pair h gets q + (h < r) of them, q = split / n_bh, r = split % n_bh); whole
+// tiles are numbered pair by pair over the rest, and split tiles pair by pair too.
+// Every pair keeps the same number of whole tiles (to within one), so with
+// xcd_remap on top an XCD's rounds of whole tiles start at pair boundaries when
+// that number is a multiple of the XCD's resident workgroups, and each round then
+// streams the K/V of a single pair through the XCD's L2. Returns
+// bh * tiles_bh + (tile within the pair); a bijection of [0, whole) and of
+// [0, split) onto the whole and the split tiles.
+__host__ __device__ __forceinline__ int plan_whole_tile(int i, int tiles_bh, int n_bh, int split) {
+  const int q = split / n_bh, r = split - q * n_bh;
+  const int few = tiles_bh - q - 1;  // whole tiles of heads h < r
+  const int a = r * few;
+  int h, t;
+  if (i < a) {
+    h = i / few;
+    t = i - h * few;
+  } else {
+    const int j = i - a, many = tiles_bh - q;
+    h = r + j / many;
+    t = j - (h - r) * many;
+  }
+  return h * tiles_bh + t;
+}
+
+__host__ __device__ __forceinline__ int plan_split_tile(int st, int tiles_bh, int n_bh, int split) {
+  const int q = split / n_bh, r = split - q * n_bh;
+  const int b = r * (q + 1);
+  int h, k;
+  if (st < b) {
+    h = st / (q + 1);
+    k = st - h * (q + 1);
+  } else {
+    const int j = st - b;
+    h = r + j / q;
+    k = j - (h - r) * q;
+  }
+  const int s_h = q + (h < r ? 1 : 0);
+  return h * tiles_bh + (tiles_bh - s_h) + k;
 }
 
 }  // namespace refadapt

@@ -207,6 +207,34 @@ def test_key_split_parity_all_elements(case, mode):
         assert max_abs(host(got.ref_mass_refq), ref["ref"]["ref_mass"]) <= MASS_TOL["bf16"]
 
 
+@pytest.mark.parametrize("mode", [("target", "cache"), ("all", "fresh")], ids=lambda m: "/".join(m))
+def test_whole_and_split_tiles_spread_over_heads(mode):
+    """A plan with whole rounds and split tiles whose count does not divide evenly over the
+    heads (5 heads; 60 or 62 query tiles each, 256 run whole, 44 or 54 split): the split
+    launch equals the unsplit one on every row, and sampled rows of every head's whole
+    and split tiles match the oracle."""
+    qset, kvsrc = mode
+    d, n_ref, n_tgt, H = 128, 300, 15360, 5
+    print(f"whole+split plan bf16 n_ref {n_ref} n_tgt {n_tgt} H {H} {qset}/{kvsrc}", flush=True)
+    assert _workspace_bytes(n_ref, n_tgt, H, d, qset, kvsrc) > 0, "the launch should split key ranges"
+    _, x = _inputs("bf16", d, n_ref, n_tgt, 1, H, seed=23)
+    got = _gpu(x, "bf16", qset, kvsrc)
+    whole = _gpu(x, "bf16", qset, kvsrc, workspace=False)
+    assert max_abs(host(got.o_tgt), host(whole.o_tgt)) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), host(whole.ref_mass)) <= MASS_TOL["bf16"]
+    if qset == "all":
+        assert max_abs(host(got.o_ref), host(whole.o_ref)) <= O_TOL["bf16"]
+    # the last 12 target tiles of a head hold its split tiles under either plan
+    rng = np.random.default_rng(5)
+    rows = np.sort(np.concatenate([rng.choice(n_tgt - 12 * 256, 24, replace=False),
+                                   n_tgt - 12 * 256 + rng.choice(12 * 256, 40, replace=False)]))
+    kr = x["k_ref_cache"] if kvsrc == "cache" else x["k_ref"]
+    vr = x["v_ref_cache"] if kvsrc == "cache" else x["v_ref"]
+    ref = joint_attention(x["q_tgt"][:, :, rows], kr, vr, x["k_tgt"], x["v_tgt"])
+    assert max_abs(host(got.o_tgt)[:, :, rows], ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass)[:, :, rows], ref["ref_mass"]) <= MASS_TOL["bf16"]
+
+
 @pytest.mark.parametrize("decision", [0, 1, 2], ids=["REUSE", "REACTIVATE", "COMPUTE"])
 def test_key_split_device_mode_follows_decision_word(decision):
     """Under RA_KV_DEVICE each decision has its own split plan, chosen on the device."""
