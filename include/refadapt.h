@@ -159,7 +159,10 @@ typedef struct {
  * segments' masses add up to ref_mass. Segment boundaries must fall on 64-row
  * key tiles (the last one is n_ref), and under RA_KV_SEGMENTS the fresh and
  * cached K (and V) views must share their strides. With seg_mass the launch
- * never splits key ranges (the workspace is not used).
+ * splits key ranges only when workspace_bytes is at least
+ * refadapt_joint_attn_seg_workspace_size(desc, n_seg) (each key chunk then
+ * records a partial log-sum-exp per segment, which the merge combines);
+ * with a smaller or no workspace it runs whole query tiles.
  *
  * Load balance (bf16): with a workspace, query tiles of a last, partly filled
  * round of workgroups are split into key-tile ranges whose partial softmax
@@ -193,6 +196,18 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
  * for an invalid desc (refadapt_joint_attn then reports the error).
  */
 size_t refadapt_joint_attn_workspace_size(const ra_attn_desc* desc);
+
+/*
+ * refadapt_joint_attn_seg_workspace_size - bytes of workspace that let a
+ * refadapt_joint_attn call with seg_mass over n_seg reference segments split
+ * key ranges for `desc` on the CURRENT device: the key-split partials plus one
+ * fp32 log-sum-exp per segment of each partial row (per-segment masses of the
+ * target queries, App. "probe non-intrusiveness and multi-reference
+ * controls"). 0 when no split pays, for an invalid desc, for n_seg outside
+ * 1..RA_MAX_SEG, and where segments are unavailable (RA_F32, RA_KV_DEVICE,
+ * n_ref == 0).
+ */
+size_t refadapt_joint_attn_seg_workspace_size(const ra_attn_desc* desc, int32_t n_seg);
 
 /*
  * refadapt_q_change - consecutive relative change of the target queries.

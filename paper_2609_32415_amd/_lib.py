@@ -36,6 +36,7 @@ RA_GATE_PRODUCT, RA_GATE_Q_ONLY, RA_GATE_MASS_ONLY, RA_GATE_AND = 0, 1, 2, 3
 EXPORTED = (
     "refadapt_joint_attn",
     "refadapt_joint_attn_workspace_size",
+    "refadapt_joint_attn_seg_workspace_size",
     "refadapt_q_change_workspace_size",
     "refadapt_q_change",
     "refadapt_gate",
@@ -133,6 +134,8 @@ def _load():
     lib.refadapt_joint_attn.restype = i32
     lib.refadapt_joint_attn_workspace_size.argtypes = [ctypes.POINTER(ra_attn_desc)]
     lib.refadapt_joint_attn_workspace_size.restype = ctypes.c_size_t
+    lib.refadapt_joint_attn_seg_workspace_size.argtypes = [ctypes.POINTER(ra_attn_desc), ctypes.c_int32]
+    lib.refadapt_joint_attn_seg_workspace_size.restype = ctypes.c_size_t
     lib.refadapt_q_change_workspace_size.argtypes = [i32, i32, i32, i32]
     lib.refadapt_q_change_workspace_size.restype = ctypes.c_size_t
     lib.refadapt_q_change.argtypes = [i32, i32, i32, i32, i32, ra_tensor, ra_tensor, f32, vp, vp, ctypes.c_size_t, vp]
@@ -192,6 +195,10 @@ def refadapt_joint_attn(desc, args, stream):
 
 def refadapt_joint_attn_workspace_size(desc):
     return int(LIB.refadapt_joint_attn_workspace_size(ctypes.byref(desc)))
+
+
+def refadapt_joint_attn_seg_workspace_size(desc, n_seg):
+    return int(LIB.refadapt_joint_attn_seg_workspace_size(ctypes.byref(desc), n_seg))
 
 
 def refadapt_q_change_workspace_size(batch, heads, n_tgt, head_dim):

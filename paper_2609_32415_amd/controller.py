@@ -679,9 +679,16 @@ def run_reference_segments(device="cuda:0", weights=(1.0, 0.5, 0.0, 1.0), sizes=
                                                   kvsrc="cache", workspace=False))
     ms_seg = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, k_cache=kc,
                                           v_cache=vc, kvsrc="segments", seg_end=ends_p, seg_cache=mixed))
+    ms_seg_cached = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, k_cache=kc,
+                                                 v_cache=vc, kvsrc="segments", seg_end=ends_p,
+                                                 seg_cache=[True] * n_seg))
+    ws_sm = ops.attn_workspace(t["q_tgt"], sum(sizes), "target", "segments", n_seg_mass=n_seg)
     ms_seg_mass = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr, k_cache=kc,
                                                v_cache=vc, kvsrc="segments", seg_end=ends_p, seg_cache=mixed,
-                                               seg_mass=True))
+                                               seg_mass=True, workspace=ws_sm))
+    ms_seg_mass_whole = timed(lambda: ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=kr, v_ref=vr,
+                                                     k_cache=kc, v_cache=vc, kvsrc="segments", seg_end=ends_p,
+                                                     seg_cache=mixed, seg_mass=True, workspace=False))
     names = [f"image{i}" for i in range(n_seg - 1)] + ["text"]
     res = {
         "segments": names, "sizes": list(sizes), "bias_weights": list(weights), "cache_noise": cache_noise,
@@ -691,7 +698,9 @@ def run_reference_segments(device="cuda:0", weights=(1.0, 0.5, 0.0, 1.0), sizes=
                               "individual_stale_impact": [round(v, 6) for v in im2],
                               "all_stale_impact": round(im_all2, 6)},
         "reuse_attention_ms": {"cache_split": round(ms_cache, 4), "cache_whole": round(ms_cache_whole, 4),
-                               "segments_mixed": round(ms_seg, 4), "segments_mixed_with_seg_mass": round(ms_seg_mass, 4)},
+                               "segments_all_cached": round(ms_seg_cached, 4),
+                               "segments_mixed": round(ms_seg, 4), "segments_mixed_with_seg_mass": round(ms_seg_mass, 4),
+                               "segments_mixed_with_seg_mass_whole": round(ms_seg_mass_whole, 4)},
     }
     if log:
         log(f"reference segments: exposure {res['exposure']}, individual stale impact "

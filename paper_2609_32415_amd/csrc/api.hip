@@ -116,9 +116,16 @@ SplitPlan plan_split(int64_t tiles, int nt, AttnSlots sl, int head_dim) {
 struct LaunchPlan {
   SplitPlan plan[2];
   int64_t qt_ref, qt_tgt;
+  int64_t items;  // split items of the larger plan
   size_t ws_bytes;
   size_t part_o_bytes;
 };
+
+// Workspace bytes of a split launch that also records per-segment masses: the partials plus
+// one log-sum-exp per segment of each partial row, after them.
+size_t seg_ws_bytes(const LaunchPlan& lp, int n_seg) {
+  return lp.ws_bytes ? lp.ws_bytes + (size_t)lp.items * kAttnBf16BM * n_seg * sizeof(float) : 0;
+}
 
 LaunchPlan plan_launch(const ra_attn_desc& d, bool split) {
   LaunchPlan lp{};
@@ -138,6 +145,7 @@ LaunchPlan plan_launch(const ra_attn_desc& d, bool split) {
   lp.plan[1] = device ? plan_split(tgt, nt, slots, d.head_dim) : lp.plan[0];
   int64_t items = 0;
   for (const SplitPlan& pl : lp.plan) items = std::max<int64_t>(items, (int64_t)pl.split_tiles * pl.chunks);
+  lp.items = items;
   lp.part_o_bytes = (size_t)items * kAttnBf16BM * d.head_dim * sizeof(float);
   lp.ws_bytes = items > 0 ? lp.part_o_bytes + (size_t)items * kAttnBf16BM * 4 * sizeof(float) : 0;
   return lp;
@@ -174,6 +182,13 @@ const char* refadapt_version(void) { return "refadapt 0.1 gfx950"; }
 size_t refadapt_joint_attn_workspace_size(const ra_attn_desc* desc) {
   if (check_attn_desc(desc, "joint_attn_workspace_size") != RA_OK) return 0;
   return plan_launch(*desc, true).ws_bytes;
+}
+
+size_t refadapt_joint_attn_seg_workspace_size(const ra_attn_desc* desc, int32_t n_seg) {
+  if (check_attn_desc(desc, "joint_attn_seg_workspace_size") != RA_OK) return 0;
+  const ra_attn_desc& d = *desc;
+  if (n_seg < 1 || n_seg > RA_MAX_SEG || d.dtype != RA_BF16 || d.kvsrc == RA_KV_DEVICE || d.n_ref < 1) return 0;
+  return seg_ws_bytes(plan_launch(d, true), n_seg);
 }
 
 ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args, void* stream) {
@@ -274,8 +289,10 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   const float scale = d.scale > 0.f ? d.scale : 1.0f / std::sqrt((float)d.head_dim);
   p.sc_log2 = scale * 1.4426950408889634f;
 
-  // Per-segment statistics need whole query tiles; per-segment sources alone may split.
-  const LaunchPlan lp = plan_launch(d, a.workspace != nullptr && a.seg_mass == nullptr);
+  // Per-segment masses split key ranges only when the workspace also holds the per-segment
+  // partials; with a smaller workspace the launch runs whole query tiles.
+  LaunchPlan lp = plan_launch(d, a.workspace != nullptr);
+  if (a.seg_mass != nullptr && a.workspace_bytes < seg_ws_bytes(lp, a.n_seg)) lp = plan_launch(d, false);
   const int64_t total = (int64_t)d.batch * d.heads * (lp.qt_ref + lp.qt_tgt);
   if (total > 0x7fffffff) return fail(RA_EUNSUPPORTED, "joint_attn: problem too large for one launch");
   if (a.workspace != nullptr) {
@@ -291,6 +308,8 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   p.plan[1] = lp.plan[1];
   p.part_o = static_cast<float*>(a.workspace);
   p.part_st = lp.ws_bytes ? reinterpret_cast<float4*>(static_cast<char*>(a.workspace) + lp.part_o_bytes) : nullptr;
+  p.part_seg = lp.ws_bytes && a.seg_mass ? reinterpret_cast<float*>(static_cast<char*>(a.workspace) + lp.ws_bytes)
+                                         : nullptr;
   if (seg) {
     p.n_seg = a.n_seg;
     for (int i = 0; i < a.n_seg; ++i) {

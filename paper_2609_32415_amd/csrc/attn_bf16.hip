@@ -259,14 +259,16 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   };
   const int qt_bh = qt_ref + p.qt_tgt;
   int tile, j0 = 0, j1 = nt, slot = -1;
+  // The segment kernel keeps the plain head-major order (split tiles last): with per-segment
+  // sources it ran 1% slower with the split tiles spread over the heads.
   if (w < pl.whole) {
-    tile = plan_whole_tile(xcd_remap(w, pl.whole), qt_bh, p.B * p.H, pl.split_tiles);
+    tile = xcd_remap(w, pl.whole);
+    if constexpr (!SEG) tile = plan_whole_tile(tile, qt_bh, p.B * p.H, pl.split_tiles);
   } else {  // key chunk c of a split tile: key tiles [c * nt / chunks, (c + 1) * nt / chunks)
-    // The chunks of neighbouring split tiles go to one XCD, as whole tiles do; both
-    // enumerations go head by head, so an XCD's chunks belong to its whole tiles' heads.
+    // The chunks of neighbouring split tiles go to one XCD, as whole tiles do.
     slot = xcd_remap(w - pl.whole, pl.total_items - pl.whole);
     const int st = slot / pl.chunks, c = slot - st * pl.chunks;
-    tile = plan_split_tile(st, qt_bh, p.B * p.H, pl.split_tiles);
+    tile = SEG ? pl.whole + st : plan_split_tile(st, qt_bh, p.B * p.H, pl.split_tiles);
     j0 = c * nt / pl.chunks;
     j1 = (c + 1) * nt / pl.chunks;
   }
@@ -432,9 +434,33 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   float m_run = -__builtin_inff(), l_run = 0.f;
   float m_ref = -__builtin_inff(), l_ref = 0.f;
   const float c = p.sc_log2;
-  // SEG: current reference segment, the key tile that ends it, and this row's seg_mass offset.
-  int seg_idx = 0, seg_end_t = SEG && n_rt > 0 ? p.seg_tile_end[0] : -1;
+  // SEG with seg_mass: the reference segment that holds this range's first key tile (a key
+  // chunk may start inside one), the key tile that ends it, this row's seg_mass offset and,
+  // for a key chunk, its row of per-segment partials.
+  int seg_idx = 0;
+  if constexpr (SEG)
+    while (seg_idx < p.n_seg && j0 >= seg_end_tab[seg_idx]) ++seg_idx;
+  const int seg_first = seg_idx;
+  int seg_end_t = SEG && seg_idx < p.n_seg ? seg_end_tab[seg_idx] : -1;
   const int64_t seg_row = ((int64_t)bh * p.n_tgt + qrow) * p.n_seg;
+  const int64_t seg_prow = ((int64_t)slot * BM + wave * 32 + n) * p.n_seg;
+  // Closes the current segment: records its log-sum-exp (log2 domain) over this key range,
+  // which the epilogue or the merge turns into a mass, then folds its sum into the reference
+  // statistics, each kept against its own max, and restarts the running sum.
+  auto close_segment = [&]() {
+    if (!ref_rows && qvalid && g == 0) {
+      const float lse_s = m_run + __log2f(l_run);
+      if (slot >= 0)
+        p.part_seg[seg_prow + seg_idx] = lse_s;
+      else
+        p.seg_mass[seg_row + seg_idx] = lse_s;
+    }
+    l_ref = seg_idx == seg_first ? l_run : l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) + l_run;
+    m_ref = m_run;
+    l_run = 0.f;
+    ++seg_idx;
+    seg_end_t = seg_idx < p.n_seg ? seg_end_tab[seg_idx] : -1;
+  };
 
   // jbc: the LDS buffer of K_j and V_j, (j - j0) & 1, as a compile-time constant.
   auto iteration = [&](auto jbc, int j, f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
@@ -636,17 +662,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     }
     l_run += xor32_add(rs_a + rs_b);
 
-    if (SEG && p.seg_mass) {  // per-segment statistics (whole tiles only)
-      if (j + 1 == seg_end_t) {  // end of reference segment seg_idx
-        // Record its log-sum-exp (log2 domain; the epilogue turns it into a mass), then
-        // fold its sum into the reference statistics, each kept against its own max.
-        if (!ref_rows && qvalid && g == 0) p.seg_mass[seg_row + seg_idx] = m_run + __log2f(l_run);
-        l_ref = seg_idx == 0 ? l_run : l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) + l_run;
-        m_ref = m_run;
-        l_run = 0.f;
-        ++seg_idx;
-        seg_end_t = seg_idx < p.n_seg ? p.seg_tile_end[seg_idx] : -1;
-      }
+    if (SEG && p.seg_mass) {  // per-segment statistics
+      if (j + 1 == seg_end_t) close_segment();  // end of reference segment seg_idx
     } else if (j == n_rt - 1) {  // end of the reference segment: freeze its statistics
       m_ref = m_run;
       l_ref = l_run;
@@ -662,9 +679,15 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
   if (j < j1) iteration(std::integral_constant<int, 0>{}, j, sa, sb);
   if (j1 < n_rt) {  // a key chunk inside the reference segment: all of it is reference mass
-    m_ref = m_run;
-    l_ref = l_run;
-    l_run = 0.f;
+    if (SEG && p.seg_mass) {
+      // The chunk ends inside a segment unless its end is a segment end: close its part.
+      const int seg_start = seg_idx > 0 ? seg_end_tab[seg_idx - 1] : 0;
+      if (max(seg_start, j0) < j1) close_segment();
+    } else {
+      m_ref = m_run;
+      l_ref = l_run;
+      l_run = 0.f;
+    }
   }
 
   // ---- epilogue of a key chunk: unnormalised output and statistics to the workspace
@@ -745,7 +768,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   const int st = r / BM, rr = r - st * BM;
   if (st >= pl.split_tiles) return;
   const int qt_bh = qt_ref + p.qt_tgt;
-  const int tile = plan_split_tile(st, qt_bh, p.B * p.H, pl.split_tiles);
+  const int tile = p.n_seg > 0 ? pl.whole + st : plan_split_tile(st, qt_bh, p.B * p.H, pl.split_tiles);
   const int bh = tile / qt_bh;
   int qt = tile - bh * qt_bh;
   const bool ref_rows = qt < qt_ref;
@@ -825,6 +848,24 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
     } else if (p.mass_refq) {
       p.mass_refq[row] = mass;
     }
+  }
+  // Per-segment masses: thread col / 4 of the row combines segment s over the chunks whose
+  // key range overlaps it, LSE_s = log2 sum_c 2^(lse_c,s), and stores 2^(LSE_s - LSE).
+  const int s = col >> 2;
+  if (p.seg_mass && !ref_rows && s < p.n_seg) {
+    const int nt = (p.n_ref + BN - 1) / BN + (p.n_tgt + BN - 1) / BN;
+    const int32_t* const ends = p.seg_tile_end;  // read through a pointer: no scratch copy
+    const int s0 = s > 0 ? ends[s - 1] : 0, s1 = ends[s];
+    const float* ps = p.part_seg + (int64_t)st * nc * BM * p.n_seg + (int64_t)rr * p.n_seg + s;
+    float Ms = -__builtin_inff();
+    for (int c = 0; c < nc; ++c)
+      if (c * nt / nc < s1 && (c + 1) * nt / nc > s0) Ms = fmaxf(Ms, ps[(int64_t)c * BM * p.n_seg]);
+    float Ls = 0.f;
+    if (Ms > -__builtin_inff())
+      for (int c = 0; c < nc; ++c)
+        if (c * nt / nc < s1 && (c + 1) * nt / nc > s0) Ls += __builtin_amdgcn_exp2f(ps[(int64_t)c * BM * p.n_seg] - Ms);
+    p.seg_mass[((int64_t)bh * p.n_tgt + qrow) * p.n_seg + s] =
+        Ls > 0.f ? __builtin_amdgcn_exp2f(Ms + __log2f(Ls) - (M + __log2f(total))) : 0.f;
   }
 }
 

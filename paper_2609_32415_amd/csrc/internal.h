@@ -22,9 +22,10 @@ enum { DEC_REUSE = 0, DEC_REACTIVATE = 1, DEC_COMPUTE = 2 };
 // Work decomposition of one bf16 attention launch over its query tiles (all
 // tiles of a (batch, head) attend to every key tile, so they cost the same).
 // Launch indices [0, whole) run whole query tiles; `split_tiles` query tiles
-// (the last ones of each (batch, head), plan_split_tile) are cut into `chunks`
-// contiguous key-tile ranges each, launched at [whole, total_items), whose
-// partial results a merge kernel combines.
+// (the last ones of each (batch, head), plan_split_tile; in the segment kernel
+// the last ones in head-major order) are cut into `chunks` contiguous key-tile
+// ranges each, launched at [whole, total_items), whose partial results a merge
+// kernel combines.
 struct SplitPlan {
   int32_t whole;        // query tiles run whole (a multiple of the resident workgroup slots)
   int32_t split_tiles;  // query tiles run in key chunks
@@ -53,7 +54,8 @@ struct AttnParams {
   SplitPlan plan[2];
   float* part_o;     // [items][BM][head_dim] unnormalised fp32 partial outputs of split items
   float4* part_st;   // [items][BM] (m, l_tgt, m_ref, l_ref) per partial row
-  // Reference segments (bf16; seg_mass needs whole tiles): n_seg > 0 selects the segment
+  float* part_seg;   // [items][BM][n_seg] per-segment log-sum-exp of partial rows (seg_mass), or null
+  // Reference segments (bf16; seg_mass splits key ranges only with part_seg): n_seg > 0 selects the segment
   // kernel. Segment s covers reference key tiles [seg_tile_end[s-1], seg_tile_end[s]);
   // seg_cache bit s reads the cached K/V for it; seg_mass [B, H, n_tgt, n_seg] or null.
   int32_t n_seg;

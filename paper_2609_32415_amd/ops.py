@@ -167,7 +167,10 @@ def joint_attn(
     shp_r = (B, H, n_ref, D)
     desc = L.ra_attn_desc(B, H, D, n_ref, n_tgt, _DTYPES[dt], float(scale or 0.0), _QSET[qset], _KVSRC[kvsrc])
     if workspace is None:
-        nbytes = L.refadapt_joint_attn_workspace_size(desc)
+        if smass_t is not None:
+            nbytes = L.refadapt_joint_attn_seg_workspace_size(desc, n_seg)
+        else:
+            nbytes = L.refadapt_joint_attn_workspace_size(desc)
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev) if nbytes else False
     if workspace is False:
         ws_ptr, ws_bytes = None, 0
@@ -202,13 +205,17 @@ def joint_attn(
     return AttnOut(o_tgt, o_ref if ref_queries else None, mass_t, lse_t, mrq_t, smass_t)
 
 
-def attn_workspace(q_tgt, n_ref, qset="target", kvsrc="fresh"):
+def attn_workspace(q_tgt, n_ref, qset="target", kvsrc="fresh", n_seg_mass=0):
     """Preallocated key-split workspace for ``joint_attn`` calls of this shape on
-    ``q_tgt``'s device (False when the library would not split)."""
+    ``q_tgt``'s device (False when the library would not split); ``n_seg_mass``
+    segments with ``seg_mass`` need the larger segment workspace."""
     B, H, n_tgt, D = q_tgt.shape
     desc = L.ra_attn_desc(B, H, D, n_ref, n_tgt, _DTYPES[q_tgt.dtype], 0.0, _QSET[qset], _KVSRC[kvsrc])
     with torch.cuda.device(q_tgt.device):
-        nbytes = L.refadapt_joint_attn_workspace_size(desc)
+        if n_seg_mass:
+            nbytes = L.refadapt_joint_attn_seg_workspace_size(desc, n_seg_mass)
+        else:
+            nbytes = L.refadapt_joint_attn_workspace_size(desc)
     return torch.empty(nbytes, dtype=torch.uint8, device=q_tgt.device) if nbytes else False
 
 

@@ -96,6 +96,18 @@ def test_joint_attn_workspace_size_needs_no_split_for_fp32_or_bad_descs():
     assert L.LIB.refadapt_joint_attn_workspace_size(None) == 0
 
 
+def test_joint_attn_seg_workspace_size_rejects_what_segments_cannot_run():
+    """The per-segment workspace query asks for nothing where segments are unavailable
+    (fp32, device mode, no reference rows) or n_seg is out of range."""
+    seg = L.RA_KV_SEGMENTS
+    assert L.refadapt_joint_attn_seg_workspace_size(_desc(kvsrc=seg), 0) == 0
+    assert L.refadapt_joint_attn_seg_workspace_size(_desc(kvsrc=seg), L.RA_MAX_SEG + 1) == 0
+    assert L.refadapt_joint_attn_seg_workspace_size(_desc(dtype=L.RA_F32, head_dim=64, kvsrc=seg), 2) == 0
+    assert L.refadapt_joint_attn_seg_workspace_size(_desc(kvsrc=L.RA_KV_DEVICE), 2) == 0
+    assert L.refadapt_joint_attn_seg_workspace_size(_desc(n_ref=0, kvsrc=seg), 2) == 0
+    assert L.LIB.refadapt_joint_attn_seg_workspace_size(None, 2) == 0
+
+
 def test_q_change_validation():
     ws = L.refadapt_q_change_workspace_size(1, 24, 4096, 128)
     assert ws >= 24 * 8 and ws % 8 == 0

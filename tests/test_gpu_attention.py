@@ -546,6 +546,69 @@ def test_reference_segments_key_split(qset):
         assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]
 
 
+def _seg_workspace_bytes(n_ref, n_tgt, H, d, qset, kvsrc, n_seg):
+    from paper_2609_32415_amd import _lib as L
+
+    desc = L.ra_attn_desc(1, H, d, n_ref, n_tgt, L.RA_BF16, 0.0, {"target": 0, "all": 1}[qset],
+                          {"fresh": 0, "cache": 1, "segments": 3}[kvsrc])
+    return L.refadapt_joint_attn_seg_workspace_size(desc, n_seg)
+
+
+SEG_SPLIT = [
+    # segment sizes, cached segments, n_tgt
+    ((256, 384, 360), (True, False, True), 100),
+    ((128,) * 8 + (40,), (True, False) * 4 + (True,), 100),
+    ((1000,), (False,), 1100),
+]
+
+
+@pytest.mark.parametrize("case", SEG_SPLIT, ids=lambda c: f"{len(c[0])}seg-{c[2]}")
+@pytest.mark.parametrize("qset", ["target", "all"])
+def test_segment_mass_key_split(case, qset):
+    """Per-segment masses with key splits: a chunk that starts or ends inside a segment
+    records a partial log-sum-exp for it, the merge combines the chunks that overlap each
+    segment; masses match the oracle and the whole-tile launch and add up to the reference
+    mass."""
+    sizes, cached, n_tgt = case
+    n_ref, n_seg = sum(sizes), len(sizes)
+    print(f"segment masses with key splits sizes {sizes} n_tgt {n_tgt} {qset}", flush=True)
+    assert _seg_workspace_bytes(n_ref, n_tgt, 2, 128, qset, "segments", n_seg) > 0, "the launch should split"
+    _, x = _inputs("bf16", 128, n_ref, n_tgt, 1, 2, seed=31)
+    kr, vr, ends = _seg_oracle_inputs(x, sizes, cached)
+    got = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached, seg_mass=True)
+    whole = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached, seg_mass=True, workspace=False)
+    ref = joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"])
+    sm = segment_masses(x["q_tgt"], kr, x["k_tgt"], ends)
+    assert max_abs(host(got.o_tgt), ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["ref_mass"]) <= MASS_TOL["bf16"]
+    lse = host(got.lse)
+    assert max_abs(lse[..., 0], ref["lse_ref"]) <= 1e-3 and max_abs(lse[..., 1], ref["lse_all"]) <= 1e-3
+    assert max_abs(host(got.seg_mass), sm) <= MASS_TOL["bf16"]
+    assert max_abs(host(got.seg_mass).sum(-1), host(got.ref_mass)) <= 1e-5
+    assert max_abs(host(got.seg_mass), host(whole.seg_mass)) <= 1e-5
+    if qset == "all":
+        rr = joint_attention(x["q_ref"], kr, vr, x["k_tgt"], x["v_tgt"])
+        assert max_abs(host(got.o_ref), rr["o"]) <= O_TOL["bf16"]
+        assert max_abs(host(got.ref_mass_refq), rr["ref_mass"]) <= MASS_TOL["bf16"]
+
+
+def test_segment_mass_with_plain_workspace_runs_whole():
+    """seg_mass with a workspace sized for the plain split runs whole query tiles (the
+    per-segment partials do not fit): results equal the whole-tile launch bitwise."""
+    from paper_2609_32415_amd import _lib as L
+
+    sizes, cached = (256, 384, 360), (True, False, True)
+    _, x = _inputs("bf16", 128, sum(sizes), 100, 1, 2, seed=31)
+    _, _, ends = _seg_oracle_inputs(x, sizes, cached)
+    desc = L.ra_attn_desc(1, 2, 128, sum(sizes), 100, L.RA_BF16, 0.0, 0, 3)
+    plain = L.refadapt_joint_attn_workspace_size(desc)
+    assert 0 < plain < L.refadapt_joint_attn_seg_workspace_size(desc, 3)
+    ws = torch.empty(plain, dtype=torch.uint8, device="cuda")
+    got = _gpu(x, "bf16", "target", "segments", seg_end=ends, seg_cache=cached, seg_mass=True, workspace=ws)
+    whole = _gpu(x, "bf16", "target", "segments", seg_end=ends, seg_cache=cached, seg_mass=True, workspace=False)
+    assert torch.equal(got.o_tgt, whole.o_tgt) and torch.equal(got.seg_mass, whole.seg_mass)
+
+
 def _random_cases(n=24, seed=2024):
     """Seeded random configurations: head dim, ragged reference/target sizes (including
     single rows and multiples of the 64-row tile), heads, batch, query set, K/V source,
