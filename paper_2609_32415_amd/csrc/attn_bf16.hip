@@ -208,7 +208,7 @@ struct DmaCursor {
 };
 
 // SEG: reference segments: each reference key tile reads the fresh or the cached K/V of its
-// segment; with seg_mass (whole tiles only) each segment's log-sum-exp is recorded.
+// segment; with seg_mass each segment's log-sum-exp over the launch's key range is recorded.
 template <int D, bool SEG>
 __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // MFMA k-steps over the head dim for S^T
