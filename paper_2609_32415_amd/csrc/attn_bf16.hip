@@ -58,7 +58,11 @@
 // key range and writes its unnormalised output with (m, l_Y, m_R, l_R) to a
 // workspace; attn_merge_kernel rescales the chunks to their common maximum and
 // sums them, which is the same reduction the online softmax performs across
-// key tiles.
+// key tiles. The split tiles are the last tiles of each (batch, head), spread
+// evenly over the heads (plan_whole_tile, plan_split_tile), so an XCD's rounds
+// of whole tiles stream few heads' K/V. With per-segment masses a chunk also
+// records one log-sum-exp per reference segment it covers, which the merge
+// combines per segment.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
