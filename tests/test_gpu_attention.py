@@ -609,7 +609,7 @@ def test_segment_mass_with_plain_workspace_runs_whole():
     assert torch.equal(got.o_tgt, whole.o_tgt) and torch.equal(got.seg_mass, whole.seg_mass)
 
 
-def _random_cases(n=24, seed=2024):
+def _random_cases(n=40, seed=2024):
     """Seeded random configurations: head dim, ragged reference/target sizes (including
     single rows and multiples of the 64-row tile), heads, batch, query set, K/V source,
     segments (with random tile-aligned boundaries and cache flags) and key splits."""
