@@ -147,7 +147,7 @@ LaunchPlan plan_launch(const ra_attn_desc& d, bool split) {
   for (const SplitPlan& pl : lp.plan) items = std::max<int64_t>(items, (int64_t)pl.split_tiles * pl.chunks);
   lp.items = items;
   lp.part_o_bytes = (size_t)items * kAttnBf16BM * d.head_dim * sizeof(float);
-  lp.ws_bytes = items > 0 ? lp.part_o_bytes + (size_t)items * kAttnBf16BM * 4 * sizeof(float) : 0;
+  lp.ws_bytes = items > 0 ? lp.part_o_bytes + (size_t)items * kAttnBf16BM * 5 * sizeof(float) : 0;
   return lp;
 }
 
@@ -308,6 +308,7 @@ ra_status refadapt_joint_attn(const ra_attn_desc* desc, const ra_attn_args* args
   p.plan[1] = lp.plan[1];
   p.part_o = static_cast<float*>(a.workspace);
   p.part_st = lp.ws_bytes ? reinterpret_cast<float4*>(static_cast<char*>(a.workspace) + lp.part_o_bytes) : nullptr;
+  p.part_lo = lp.ws_bytes ? reinterpret_cast<float*>(p.part_st + lp.items * kAttnBf16BM) : nullptr;
   p.part_seg = lp.ws_bytes && a.seg_mass ? reinterpret_cast<float*>(static_cast<char*>(a.workspace) + lp.ws_bytes)
                                          : nullptr;
   if (seg) {

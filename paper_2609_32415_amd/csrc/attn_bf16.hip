@@ -42,7 +42,11 @@
 // the scores still to be formed, rescales O and l, and forms them again. The
 // O rescale and the row max are thus almost never executed.
 // Row sums add the fp32 probabilities, so the reference mass and the
-// log-sum-exp carry no bf16 rounding.
+// log-sum-exp carry no bf16 rounding. O is divided by a second sum, that of
+// the bf16-rounded probabilities it accumulated (one v_dot2c_f32_bf16 per
+// packed pair, in MFMA slots that form no probabilities), so the weights
+// applied to V sum to one: with the fp32 sum, the rounding of a dominant
+// probability (relative error up to 2^-8) moved the output by as much of V.
 //
 // Split statistics for the reference mass (paper Sec. 3.2, directional
 // exposure): after the last reference tile the running (max, sum) pair is
@@ -101,6 +105,12 @@ __device__ __forceinline__ float xor32_max(float v) {
 __device__ __forceinline__ float xor32_add(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// acc + lo + hi of a packed pair of bf16 values (one v_dot2c_f32_bf16 against (1, 1)).
+__device__ __forceinline__ float add_bf16x2(uint32_t w, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), one, acc, false);
 }
 
 // Keeps a value in a register at this point of the program, so the optimizer
@@ -436,6 +446,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x16{};
   float m_run = -__builtin_inff(), l_run = 0.f;
+  // Sum of the bf16-rounded probabilities that enter O (this lane's keys, against m_run): the
+  // output is normalised by it, so the weights applied to V sum to one (l_run, the fp32 sum,
+  // gives the mass and the log-sum-exp).
+  float lo_run = 0.f;
   float m_ref = -__builtin_inff(), l_ref = 0.f;
   const float c = p.sc_log2;
   // SEG with seg_mass: the reference segment that holds this range's first key tile (a key
@@ -503,6 +517,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     uint32_t pw[4][4];  // packed bf16 probabilities: P block s2, keys 16*s2 + 8*g + 2w, +1
     // Row-sum chains: pairs 0..7 (P blocks 0, 1) and pairs 8..15 (P blocks 2, 3).
     float rs_a = 0.f, rs_b = 0.f, m_new = m_run;
+    float lo_t = 0.f;  // this tile's rounded-probability sum (P blocks 0, 1, then 2, 3)
     auto prob_pair = [&](int q) {  // scores 2q, 2q+1 -> P block q/4, word q%4
       const int mb = q >> 3, o2 = (2 * q) & 15;
       const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m_new));
@@ -520,6 +535,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       uint32_t w = __builtin_bit_cast(uint32_t, pr);
       pin(w);
       pw[q >> 2][q & 3] = w;
+      if (q < 8) lo_t = add_bf16x2(w, lo_t);  // cold path: P blocks 0 and 1 formed again
     };
     // Software pipeline of the pairs over the MFMA slots: a slot forms the exponent
     // arguments of pair k, the exponentials of pair k - 1 and the row-sum adds and bf16 pack
@@ -582,20 +598,32 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       s_next[i / KS] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i & 3], qreg[i % KS], s_next[i / KS], 0, 0, 0);
       if (i + 4 < NQK) ka[i & 3] = k_operand(i + 4);
       if (i < 12) pipe_slot(i, 0, 10);  // pairs 0..9: P blocks 0, 1 and half of block 2
+      // The last four slots hold no pair: the rounded sum of P blocks 0 and 1 (formed
+      // again, sum included, if the bound test below fails).
+      if (i >= 12) {
+        lo_t = add_bf16x2(pw[(i - 12) >> 1][2 * (i & 1)], lo_t);
+        lo_t = add_bf16x2(pw[(i - 12) >> 1][2 * (i & 1) + 1], lo_t);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int k = NQK; k < 12; ++k) pipe_slot(k, 0, 10);  // head_dim 64: fewer MFMAs than slots
+    if constexpr (NQK < 16) {  // head_dim 64: no spare slots
+#pragma unroll
+      for (int wd = 0; wd < 8; ++wd) lo_t = add_bf16x2(pw[wd >> 2][wd & 3], lo_t);
+    }
     if (__any(!(rs_a + rs_b <= PBOUND))) {
       // Rare (always at a workgroup's first tile): move the max to the tile's row max
       // (nothing of this tile is in O^T yet) and form pairs 0..9 again.
       m_new = fmaxf(tile_max(0), m_run);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
+      lo_run *= alpha;
 #pragma unroll
       for (int i = 0; i < DB; ++i) o[i] *= alpha;
       m_run = m_new;
       rs_a = rs_b = 0.f;
+      lo_t = 0.f;
 #pragma unroll
       for (int q = 0; q < 10; ++q) prob_pair(q);
     }
@@ -646,6 +674,15 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         prob_pair(10 + 2 * i);
         prob_pair(11 + 2 * i);
       }
+      // Rounded sum of P blocks 2 and 3 (final after the check below) under the MFMAs that
+      // form no probabilities.
+      if (i >= 2 * DB) {
+#pragma unroll
+        for (int u = 0; u < 4 / DB; ++u) {
+          const int wd = (i - 2 * DB) * (4 / DB) + u;  // word 0..7 of blocks 2 and 3
+          lo_t = add_bf16x2(pw[2 + (wd >> 2)][wd & 3], lo_t);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
       if (i == 2 * DB - 1 && __any(!(rs_b <= PBOUND))) {
         // Rare: pairs 8..15 exceed the bound. O^T holds this tile's P blocks 0 and 1
@@ -655,6 +692,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         m_new = fmaxf(tile_max(1), m_run);
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         l_run *= alpha;
+        lo_run *= alpha;
+        lo_t *= alpha;
         rs_a *= alpha;
 #pragma unroll
         for (int k = 0; k < DB; ++k) o[k] *= alpha;
@@ -665,6 +704,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       }
     }
     l_run += xor32_add(rs_a + rs_b);
+    lo_run += lo_t;
 
     if (SEG && p.seg_mass) {  // per-segment statistics
       if (j + 1 == seg_end_t) close_segment();  // end of reference segment seg_idx
@@ -694,6 +734,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     }
   }
 
+  const float lo_sum = xor32_add(lo_run);  // both lanes of a query hold half its keys
   // ---- epilogue of a key chunk: unnormalised output and statistics to the workspace
   if (slot >= 0) {
     if (qvalid) {
@@ -705,7 +746,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         for (int rr = 0; rr < 4; ++rr)
           *reinterpret_cast<float4*>(po + 32 * db + 8 * rr + 4 * g) =
               float4{o[db][4 * rr], o[db][4 * rr + 1], o[db][4 * rr + 2], o[db][4 * rr + 3]};
-      if (g == 0) p.part_st[prow] = float4{m_run, l_run, m_ref, l_ref};
+      if (g == 0) {
+        p.part_st[prow] = float4{m_run, l_run, m_ref, l_ref};
+        p.part_lo[prow] = lo_sum;
+      }
     }
     probe_end();
     return;
@@ -715,6 +759,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   const float L_R = l_ref > 0.f ? l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) : 0.f;
   const float total = L_R + l_run;
   const float inv = 1.f / total;
+  const float inv_o = 1.f / lo_sum;
   if (qvalid) {
     uint16_t* op = static_cast<uint16_t*>(const_cast<void*>(ov.p)) + b * ov.sb + h * ov.sh + (int64_t)qrow * ov.ss;
 #pragma unroll
@@ -726,7 +771,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
           u32x2 w;
         } pk;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pk.h[i] = (__bf16)(o[db][4 * rr + i] * inv);
+        for (int i = 0; i < 4; ++i) pk.h[i] = (__bf16)(o[db][4 * rr + i] * inv_o);
         *reinterpret_cast<u32x2*>(op + 32 * db + 8 * rr + 4 * g) = pk.w;
       }
     if (g == 0) {
@@ -800,14 +845,17 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
     }
   }
   float L_Rr = 0.f, L_Y = 0.f;  // L_Rr: reference sum against M_R
+  float L_o = 0.f;              // sum of the rounded probabilities that entered O
   float4 acc{0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < nc; c0 += MERGE_BATCH) {
     float4 sv[MERGE_BATCH], ov[MERGE_BATCH];
+    float lv[MERGE_BATCH];
 #pragma unroll
     for (int u = 0; u < MERGE_BATCH; ++u) {
       if (c0 + u < nc) {
         const int64_t prow = base + (int64_t)(c0 + u) * BM;
         sv[u] = p.part_st[prow];
+        lv[u] = p.part_lo[prow];
         ov[u] = *reinterpret_cast<const float4*>(p.part_o + prow * D + col);
       }
     }
@@ -816,6 +864,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
       if (c0 + u < nc) {
         const float wgt = __builtin_amdgcn_exp2f(sv[u].x - M);
         L_Y += sv[u].y * wgt;
+        L_o += lv[u] * wgt;
         if (sv[u].w > 0.f) L_Rr += sv[u].w * __builtin_amdgcn_exp2f(sv[u].z - M_R);
         acc.x += ov[u].x * wgt;
         acc.y += ov[u].y * wgt;
@@ -826,7 +875,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
   }
   const float L_R = L_Rr > 0.f ? L_Rr * __builtin_amdgcn_exp2f(M_R - M) : 0.f;
   const float total = L_R + L_Y;
-  const float inv = 1.f / total;
+  const float inv = 1.f / total, inv_o = 1.f / L_o;
   const View ov = ref_rows ? p.o_ref : p.o_tgt;
   const int b = bh / p.H, h = bh - b * p.H;
   uint16_t* op = static_cast<uint16_t*>(const_cast<void*>(ov.p)) + b * ov.sb + h * ov.sh + (int64_t)qrow * ov.ss;
@@ -834,10 +883,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
     __bf16 h[4];
     u32x2 w;
   } pk;
-  pk.h[0] = (__bf16)(acc.x * inv);
-  pk.h[1] = (__bf16)(acc.y * inv);
-  pk.h[2] = (__bf16)(acc.z * inv);
-  pk.h[3] = (__bf16)(acc.w * inv);
+  pk.h[0] = (__bf16)(acc.x * inv_o);
+  pk.h[1] = (__bf16)(acc.y * inv_o);
+  pk.h[2] = (__bf16)(acc.z * inv_o);
+  pk.h[3] = (__bf16)(acc.w * inv_o);
   *reinterpret_cast<u32x2*>(op + col) = pk.w;
   if (col == 0) {
     const float mass = L_R * inv;

@@ -54,6 +54,7 @@ struct AttnParams {
   SplitPlan plan[2];
   float* part_o;     // [items][BM][head_dim] unnormalised fp32 partial outputs of split items
   float4* part_st;   // [items][BM] (m, l_tgt, m_ref, l_ref) per partial row
+  float* part_lo;    // [items][BM] sum of the bf16-rounded probabilities of a partial row
   float* part_seg;   // [items][BM][n_seg] per-segment log-sum-exp of partial rows (seg_mass), or null
   // Reference segments (bf16; seg_mass splits key ranges only with part_seg): n_seg > 0 selects the segment
   // kernel. Segment s covers reference key tiles [seg_tile_end[s-1], seg_tile_end[s]);
