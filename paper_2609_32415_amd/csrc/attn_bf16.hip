@@ -44,7 +44,7 @@
 // Row sums add the fp32 probabilities, so the reference mass and the
 // log-sum-exp carry no bf16 rounding. O is divided by a second sum, that of
 // the bf16-rounded probabilities it accumulated (one v_dot2c_f32_bf16 per
-// packed pair, in MFMA slots that form no probabilities), so the weights
+// packed pair, after the tile's last MFMA), so the weights
 // applied to V sum to one: with the fp32 sum, the rounding of a dominant
 // probability (relative error up to 2^-8) moved the output by as much of V.
 //
@@ -107,17 +107,17 @@ __device__ __forceinline__ float xor32_add(float v) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// acc + lo + hi of a packed pair of bf16 values (one v_dot2c_f32_bf16 against (1, 1)).
-__device__ __forceinline__ float add_bf16x2(uint32_t w, float acc) {
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), one, acc, false);
-}
-
 // Keeps a value in a register at this point of the program, so the optimizer
 // cannot sink the instructions that produce it into a later block.
 template <typename T>
 __device__ __forceinline__ void pin(T& v) {
   asm volatile("" : "+v"(v));
+}
+
+// acc + lo + hi of a packed pair of bf16 values (one v_dot2c_f32_bf16 against (1, 1)).
+__device__ __forceinline__ float add_bf16x2(uint32_t w, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), one, acc, false);
 }
 
 // LDS tiles are filled by direct global-to-LDS loads (buffer_load_dwordx4 ... lds):
@@ -517,7 +517,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     uint32_t pw[4][4];  // packed bf16 probabilities: P block s2, keys 16*s2 + 8*g + 2w, +1
     // Row-sum chains: pairs 0..7 (P blocks 0, 1) and pairs 8..15 (P blocks 2, 3).
     float rs_a = 0.f, rs_b = 0.f, m_new = m_run;
-    float lo_t = 0.f;  // this tile's rounded-probability sum (P blocks 0, 1, then 2, 3)
+    float a01 = 1.f;  // rescale of P blocks 0 and 1 by the second bound test
     auto prob_pair = [&](int q) {  // scores 2q, 2q+1 -> P block q/4, word q%4
       const int mb = q >> 3, o2 = (2 * q) & 15;
       const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m_new));
@@ -535,7 +535,6 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       uint32_t w = __builtin_bit_cast(uint32_t, pr);
       pin(w);
       pw[q >> 2][q & 3] = w;
-      if (q < 8) lo_t = add_bf16x2(w, lo_t);  // cold path: P blocks 0 and 1 formed again
     };
     // Software pipeline of the pairs over the MFMA slots: a slot forms the exponent
     // arguments of pair k, the exponentials of pair k - 1 and the row-sum adds and bf16 pack
@@ -598,20 +597,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       s_next[i / KS] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[i & 3], qreg[i % KS], s_next[i / KS], 0, 0, 0);
       if (i + 4 < NQK) ka[i & 3] = k_operand(i + 4);
       if (i < 12) pipe_slot(i, 0, 10);  // pairs 0..9: P blocks 0, 1 and half of block 2
-      // The last four slots hold no pair: the rounded sum of P blocks 0 and 1 (formed
-      // again, sum included, if the bound test below fails).
-      if (i >= 12) {
-        lo_t = add_bf16x2(pw[(i - 12) >> 1][2 * (i & 1)], lo_t);
-        lo_t = add_bf16x2(pw[(i - 12) >> 1][2 * (i & 1) + 1], lo_t);
-      }
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int k = NQK; k < 12; ++k) pipe_slot(k, 0, 10);  // head_dim 64: fewer MFMAs than slots
-    if constexpr (NQK < 16) {  // head_dim 64: no spare slots
-#pragma unroll
-      for (int wd = 0; wd < 8; ++wd) lo_t = add_bf16x2(pw[wd >> 2][wd & 3], lo_t);
-    }
     if (__any(!(rs_a + rs_b <= PBOUND))) {
       // Rare (always at a workgroup's first tile): move the max to the tile's row max
       // (nothing of this tile is in O^T yet) and form pairs 0..9 again.
@@ -623,7 +612,6 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       for (int i = 0; i < DB; ++i) o[i] *= alpha;
       m_run = m_new;
       rs_a = rs_b = 0.f;
-      lo_t = 0.f;
 #pragma unroll
       for (int q = 0; q < 10; ++q) prob_pair(q);
     }
@@ -674,15 +662,6 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         prob_pair(10 + 2 * i);
         prob_pair(11 + 2 * i);
       }
-      // Rounded sum of P blocks 2 and 3 (final after the check below) under the MFMAs that
-      // form no probabilities.
-      if (i >= 2 * DB) {
-#pragma unroll
-        for (int u = 0; u < 4 / DB; ++u) {
-          const int wd = (i - 2 * DB) * (4 / DB) + u;  // word 0..7 of blocks 2 and 3
-          lo_t = add_bf16x2(pw[2 + (wd >> 2)][wd & 3], lo_t);
-        }
-      }
       __builtin_amdgcn_sched_barrier(0);
       if (i == 2 * DB - 1 && __any(!(rs_b <= PBOUND))) {
         // Rare: pairs 8..15 exceed the bound. O^T holds this tile's P blocks 0 and 1
@@ -693,7 +672,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         l_run *= alpha;
         lo_run *= alpha;
-        lo_t *= alpha;
+        a01 = alpha;
         rs_a *= alpha;
 #pragma unroll
         for (int k = 0; k < DB; ++k) o[k] *= alpha;
@@ -704,7 +683,19 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       }
     }
     l_run += xor32_add(rs_a + rs_b);
-    lo_run += lo_t;
+    // The rounded sum of the tile's P after its last MFMA has issued: in the MFMA slots the
+    // dot2 instructions slowed the matrix core's issue (+8% against +2.5% here).
+    __builtin_amdgcn_sched_barrier(0);
+    {
+      float s01 = 0.f, s23 = 0.f;
+#pragma unroll
+      for (int wd = 0; wd < 8; ++wd) {
+        s01 = add_bf16x2(pw[wd >> 2][wd & 3], s01);
+        s23 = add_bf16x2(pw[2 + (wd >> 2)][wd & 3], s23);
+      }
+      lo_run += s01 * a01 + s23;
+      pin(lo_run);
+    }
 
     if (SEG && p.seg_mass) {  // per-segment statistics
       if (j + 1 == seg_end_t) close_segment();  // end of reference segment seg_idx
