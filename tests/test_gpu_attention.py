@@ -435,6 +435,45 @@ def _jump_inputs(d, pattern, n_ref=600, n_tgt=300, H=2, seed=11):
     return {k: synth.round_to_dtype(v, "bf16") for k, v in x.items()}
 
 
+def _dominant_key_inputs(b, vscale, d=128, n_ref=300, n_tgt=400, H=2, seed=41):
+    """One target key per head scores about 2b/sqrt(d) log2 units above the reference keys
+    (every query gets a component 2u, the key b u): far enough to dominate its rows, not far
+    enough to move the running max (its probability stays below the rescale bound), so the
+    bf16 rounding of that one probability decides the output. Its value row is +-vscale."""
+    _, x = _inputs("bf16", d, n_ref, n_tgt, 1, H, seed=seed, bias=False)
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    x = {k: v.astype(np.float64) for k, v in x.items()}
+    for k in ("q_tgt", "q_ref"):
+        x[k] = x[k] + 2.0 * u
+    idx = 2 * 64 + 17
+    x["k_tgt"][:, :, idx, :] += b * u
+    x["v_tgt"][:, :, idx, :] = vscale * np.sign(rng.standard_normal((1, H, d)))
+    x["k_ref_cache"], x["v_ref_cache"] = x["k_ref"], x["v_ref"]
+    return {k: synth.round_to_dtype(v, "bf16") for k, v in x.items()}
+
+
+@pytest.mark.parametrize("b", [30.0, 40.0])
+@pytest.mark.parametrize("mode", [("target", "fresh"), ("all", "fresh")], ids=lambda m: "/".join(m))
+@pytest.mark.parametrize("split", [True, False], ids=["split", "whole"])
+def test_dominant_key_below_the_rescale_bound(b, mode, split):
+    """A dominant key whose probability is not rounded at 1 (the running max stays at the
+    reference keys): outputs of magnitude up to 2.5 stay within the 1e-2 bar, which holds
+    because O is divided by the sum of the rounded probabilities it accumulated."""
+    qset, kvsrc = mode
+    print(f"dominant key b={b} {qset}/{kvsrc} split={split}", flush=True)
+    x = _dominant_key_inputs(b, 2.5)
+    got = _gpu(x, "bf16", qset, kvsrc, **({} if split else {"workspace": False}))
+    ref = _oracle(x, qset, False)
+    err = max_abs(host(got.o_tgt), ref["tgt"]["o"])
+    print(f"  max|o| {np.abs(ref['tgt']['o']).max():.3f} max|dO| {err:.5f}", flush=True)
+    assert err <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    if qset == "all":
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
+
+
 @pytest.mark.parametrize("d", [128, 64])
 @pytest.mark.parametrize("pattern", ["spikes", "ramp", "huge"])
 @pytest.mark.parametrize("mode", [("target", "fresh"), ("all", "fresh")], ids=lambda m: "/".join(m))
