@@ -445,6 +445,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   f32x16 o[DB];
 #pragma unroll
   for (int i = 0; i < DB; ++i) o[i] = f32x16{};
+  // l_run and l_ref hold this lane's half of the query's keys (its partner lane l ^ 32 the
+  // other half; both see the same max): the halves are added where a whole sum is read.
   float m_run = -__builtin_inff(), l_run = 0.f;
   // Sum of the bf16-rounded probabilities that enter O (this lane's keys, against m_run): the
   // output is normalised by it, so the weights applied to V sum to one (l_run, the fp32 sum,
@@ -466,8 +468,9 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   // which the epilogue or the merge turns into a mass, then folds its sum into the reference
   // statistics, each kept against its own max, and restarts the running sum.
   auto close_segment = [&]() {
+    const float l_seg = xor32_add(l_run);  // whole wavefront: the swap reads the partner lane
     if (!ref_rows && qvalid && g == 0) {
-      const float lse_s = m_run + __log2f(l_run);
+      const float lse_s = m_run + __log2f(l_seg);
       if (slot >= 0)
         p.part_seg[seg_prow + seg_idx] = lse_s;
       else
@@ -518,17 +521,22 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // Row-sum chains: pairs 0..7 (P blocks 0, 1) and pairs 8..15 (P blocks 2, 3).
     float rs_a = 0.f, rs_b = 0.f, m_new = m_run;
     float a01 = 1.f;  // rescale of P blocks 0 and 1 by the second bound test
+    // Adds a pair to its row-sum chain; the first pair of a chain starts it (0 + x is not
+    // folded away: it would turn -0 into +0).
+    auto row_add = [&](int q, float e0, float e1) {
+      if (q < 8) {
+        rs_a = q == 0 ? e0 + e1 : rs_a + (e0 + e1);
+        pin(rs_a);
+      } else {
+        rs_b = q == 8 ? e0 + e1 : rs_b + (e0 + e1);
+        pin(rs_b);
+      }
+    };
     auto prob_pair = [&](int q) {  // scores 2q, 2q+1 -> P block q/4, word q%4
       const int mb = q >> 3, o2 = (2 * q) & 15;
       const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m_new));
       const float e1 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2 + 1], c, -m_new));
-      if (q < 8) {
-        rs_a += e0 + e1;
-        pin(rs_a);
-      } else {
-        rs_b += e0 + e1;
-        pin(rs_b);
-      }
+      row_add(q, e0, e1);
       bf16x2 pr;
       pr[0] = (__bf16)e0;
       pr[1] = (__bf16)e1;
@@ -542,13 +550,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     float pa0 = 0.f, pa1 = 0.f;  // exponent arguments of the pair started one slot earlier
     float pe0 = 0.f, pe1 = 0.f;  // exponentials of the pair started two slots earlier
     auto pair_fin = [&](int q) {
-      if (q < 8) {
-        rs_a += pe0 + pe1;
-        pin(rs_a);
-      } else {
-        rs_b += pe0 + pe1;
-        pin(rs_b);
-      }
+      row_add(q, pe0, pe1);
       bf16x2 pr;
       pr[0] = (__bf16)pe0;
       pr[1] = (__bf16)pe1;
@@ -575,6 +577,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // Row max of the lane's scores in key blocks mb0..1, shared by the lane pair of a query.
     auto tile_max = [&](int mb0) {
       float m = s_cur[1][0];
+      pin(m);  // keeps the reduction in the cold path (it was otherwise begun in the hot block)
 #pragma unroll
       for (int r = 1; r < 16; ++r) m = fmaxf(m, s_cur[1][r]);
       if (mb0 == 0) {
@@ -682,7 +685,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         for (int q = 8; q < 16; ++q) prob_pair(q);
       }
     }
-    l_run += xor32_add(rs_a + rs_b);
+    l_run += rs_a + rs_b;
     // The rounded sum of the tile's P after its last MFMA has issued: in the MFMA slots the
     // dot2 instructions slowed the matrix core's issue (+8% against +2.5% here).
     __builtin_amdgcn_sched_barrier(0);
@@ -726,6 +729,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
 
   const float lo_sum = xor32_add(lo_run);  // both lanes of a query hold half its keys
+  const float l_sum = xor32_add(l_run), l_ref_sum = xor32_add(l_ref);
   // ---- epilogue of a key chunk: unnormalised output and statistics to the workspace
   if (slot >= 0) {
     if (qvalid) {
@@ -738,7 +742,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
           *reinterpret_cast<float4*>(po + 32 * db + 8 * rr + 4 * g) =
               float4{o[db][4 * rr], o[db][4 * rr + 1], o[db][4 * rr + 2], o[db][4 * rr + 3]};
       if (g == 0) {
-        p.part_st[prow] = float4{m_run, l_run, m_ref, l_ref};
+        p.part_st[prow] = float4{m_run, l_sum, m_ref, l_ref_sum};
         p.part_lo[prow] = lo_sum;
       }
     }
@@ -747,8 +751,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
 
   // ---- epilogue
-  const float L_R = l_ref > 0.f ? l_ref * __builtin_amdgcn_exp2f(m_ref - m_run) : 0.f;
-  const float total = L_R + l_run;
+  const float L_R = l_ref_sum > 0.f ? l_ref_sum * __builtin_amdgcn_exp2f(m_ref - m_run) : 0.f;
+  const float total = L_R + l_sum;
   const float inv = 1.f / total;
   const float inv_o = 1.f / lo_sum;
   if (qvalid) {
@@ -772,7 +776,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
         if (p.mass_tgt) p.mass_tgt[row] = mass;
         if (p.lse_tgt) {
           const float ln2 = 0.69314718055994531f;
-          p.lse_tgt[2 * row] = (m_ref + __log2f(l_ref)) * ln2;
+          p.lse_tgt[2 * row] = (m_ref + __log2f(l_ref_sum)) * ln2;
           p.lse_tgt[2 * row + 1] = (m_run + __log2f(total)) * ln2;
         }
       } else if (p.mass_refq) {
