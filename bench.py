@@ -13,8 +13,10 @@ thresholds (inf, 0, 0) make the three blocks take the three decisions:
            the commit copies the fresh reference Q/K/V into the block cache   (3.402 TFLOP)
 
 Every launch reads its decision word on the device (no host round-trip).
-``value`` = attention FLOPs of the three blocks / measured step time. The JSON
-line also carries each phase's mean / median / min, each attention mode on its
+``value`` = attention FLOPs of the three blocks / measured step time, timed over
+K steps with nothing else on the stream; a second pass of K steps records an
+event between phases and runs the clock probes. The JSON line also carries
+each phase's mean / median / min (second pass), each attention mode on its
 own, the mean shader clock over the COMPUTE block's attention launches (an
 in-kernel probe) and the fraction of peak at that clock, the roofline of the
 dominant kernel (the COMPUTE block's attention) measured live with HIP events
@@ -302,18 +304,25 @@ def main():
     torch.cuda.synchronize()
     dec = ctl.decisions[1].cpu().tolist()
     assert dec == [ops.REUSE, ops.REACTIVATE, ops.COMPUTE], f"bench step decisions {dec}"
-    for v in probe.values():
-        v.zero_()
+    # The timed pass: K steps with nothing but the path on the stream. A second pass of K
+    # steps records an event between phases and runs the clock probes, for the per-phase
+    # figures and the shader clock only.
     t0, t1 = ev(), ev()
-    pending = []
     torch.cuda.synchronize()
     t0.record()
     for i in range(args.steps):
-        pending.append(step(args.warmup + i, True))  # the input sets keep alternating
+        step(args.warmup + i, False)  # the input sets keep alternating
     t1.record()
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     ms_per_step = total_ms / args.steps
+    assert ctl.decisions[1].cpu().tolist() == [ops.REUSE, ops.REACTIVATE, ops.COMPUTE]
+    for v in probe.values():
+        v.zero_()
+    pending = []
+    for i in range(args.steps):
+        pending.append(step(args.warmup + args.steps + i, True))
+    torch.cuda.synchronize()
     assert ctl.decisions[1].cpu().tolist() == [ops.REUSE, ops.REACTIVATE, ops.COMPUTE]
     # phases: per block gate, attn, commit (events 1 + 3 b + k)
     phase = {}
