@@ -305,6 +305,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   int64_t kr_ss = krv.ss, vr_ss = vrv.ss, ky_ss = p.k_tgt.ss, vy_ss = p.v_tgt.ss;
 
   auto tile_valid = [&](int j) { return j < n_rt ? min(BN, p.n_ref - j * BN) : min(BN, p.n_tgt - (j - n_rt) * BN); };
+  const int rag_ref = p.n_ref % BN ? n_rt - 1 : -1;  // key tiles with fewer than BN keys
+  const int rag_tgt = p.n_tgt % BN ? nt - 1 : -1;
   // Per-lane byte offsets of the direct loads, per source view (the segments of SEG share
   // the reference views' strides).
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -494,8 +496,10 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     uint16_t* const vb_cur = jb ? vbuf1 : vbuf0;   // V_j
     uint16_t* const vb_next = jb ? vbuf0 : vbuf1;  // V_{j-1} (already read), refilled with V_{j+1}
 
-    const int valid = tile_valid(j);
-    if (valid < BN) {  // ragged last tile of a segment: drop keys past its end
+    // The ragged last tile of each of the reference and target segments (if any) is known
+    // up front: the test in the loop compares tile indices only.
+    if (j == rag_ref || j == rag_tgt) {  // ragged last tile of a segment: drop keys past its end
+      const int valid = tile_valid(j);
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
