@@ -222,8 +222,10 @@ struct DmaCursor {
 };
 
 // SEG: reference segments: each reference key tile reads the fresh or the cached K/V of its
-// segment; with seg_mass each segment's log-sum-exp over the launch's key range is recorded.
-template <int D, bool SEG>
+// segment. SEGM (with SEG, for a non-null seg_mass): each segment's log-sum-exp over the
+// launch's key range is recorded; an instance of its own, so that launches without it carry
+// none of its state (2% of the segment launch).
+template <int D, bool SEG, bool SEGM>
 __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   constexpr int KS = D / 16;   // MFMA k-steps over the head dim for S^T
   constexpr int DB = D / 32;   // 32-row blocks of the O^T accumulator
@@ -704,7 +706,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       pin(lo_run);
     }
 
-    if (SEG && p.seg_mass) {  // per-segment statistics
+    if (SEGM) {  // per-segment statistics
       if (j + 1 == seg_end_t) close_segment();  // end of reference segment seg_idx
     } else if (j == n_rt - 1) {  // end of the reference segment: freeze its statistics
       m_ref = m_run;
@@ -721,7 +723,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
   }
   if (j < j1) iteration(std::integral_constant<int, 0>{}, j, sa, sb);
   if (j1 < n_rt) {  // a key chunk inside the reference segment: all of it is reference mass
-    if (SEG && p.seg_mass) {
+    if (SEGM) {
       // The chunk ends inside a segment unless its end is a segment end: close its part.
       const int seg_start = seg_idx > 0 ? seg_end_tab[seg_idx - 1] : 0;
       if (max(seg_start, j0) < j1) close_segment();
@@ -786,7 +788,7 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
       } else if (p.mass_refq) {
         p.mass_refq[row] = mass;
       }
-      if (SEG && p.seg_mass && !ref_rows) {  // per-segment log-sum-exp -> mass, in place
+      if (SEGM && !ref_rows) {  // per-segment log-sum-exp -> mass, in place
         const float lt = m_run + __log2f(total);
         for (int s2 = 0; s2 < p.n_seg; ++s2)
           p.seg_mass[seg_row + s2] = __builtin_amdgcn_exp2f(p.seg_mass[seg_row + s2] - lt);
@@ -923,10 +925,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
 
 // Explicit instantiations: without them the host pass leaves the segment instances, which
 // are only reached through the launcher's kernel-pointer argument, without launch stubs.
-template __global__ void attn_bf16_kernel<128, false>(AttnParams);
-template __global__ void attn_bf16_kernel<64, false>(AttnParams);
-template __global__ void attn_bf16_kernel<128, true>(AttnParams);
-template __global__ void attn_bf16_kernel<64, true>(AttnParams);
+template __global__ void attn_bf16_kernel<128, false, false>(AttnParams);
+template __global__ void attn_bf16_kernel<64, false, false>(AttnParams);
+template __global__ void attn_bf16_kernel<128, true, false>(AttnParams);
+template __global__ void attn_bf16_kernel<64, true, false>(AttnParams);
+template __global__ void attn_bf16_kernel<128, true, true>(AttnParams);
+template __global__ void attn_bf16_kernel<64, true, true>(AttnParams);
 
 }  // namespace
 
@@ -942,8 +946,8 @@ AttnSlots attn_bf16_slots(int head_dim) {
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return AttnSlots{0, 0};
   const hipError_t e =
       head_dim == 128
-          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<128, false>, NT, 0)
-          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<64, false>, NT, 0);
+          ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<128, false, false>, NT, 0)
+          : hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, attn_bf16_kernel<64, false, false>, NT, 0);
   if (e != hipSuccess || per_cu < 1 || cus < 1) return AttnSlots{0, 0};
   if (dev < 64) {
     cache[dev][di][1].store(per_cu, std::memory_order_relaxed);
@@ -957,12 +961,16 @@ hipError_t launch_attn_bf16(const AttnParams& p, int head_dim, hipStream_t strea
   if (items <= 0) return hipSuccess;
   const dim3 grid(items), block(NT);
   hipError_t e;
-  if (p.n_seg > 0)
-    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, true>, grid, block, 0, stream, p)
-                        : launch_kernel(attn_bf16_kernel<64, true>, grid, block, 0, stream, p);
-  else
-    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, false>, grid, block, 0, stream, p)
-                        : launch_kernel(attn_bf16_kernel<64, false>, grid, block, 0, stream, p);
+  if (p.n_seg > 0 && p.seg_mass) {
+    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, true, true>, grid, block, 0, stream, p)
+                        : launch_kernel(attn_bf16_kernel<64, true, true>, grid, block, 0, stream, p);
+  } else if (p.n_seg > 0) {
+    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, true, false>, grid, block, 0, stream, p)
+                        : launch_kernel(attn_bf16_kernel<64, true, false>, grid, block, 0, stream, p);
+  } else {
+    e = head_dim == 128 ? launch_kernel(attn_bf16_kernel<128, false, false>, grid, block, 0, stream, p)
+                        : launch_kernel(attn_bf16_kernel<64, false, false>, grid, block, 0, stream, p);
+  }
   if (e != hipSuccess) return e;
   const int split = max(p.plan[0].split_tiles, p.plan[1].split_tiles);
   if (split == 0) return hipSuccess;
