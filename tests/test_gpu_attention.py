@@ -603,16 +603,17 @@ SEG_SPLIT = [
 
 @pytest.mark.parametrize("case", SEG_SPLIT, ids=lambda c: f"{len(c[0])}seg-{c[2]}")
 @pytest.mark.parametrize("qset", ["target", "all"])
-def test_segment_mass_key_split(case, qset):
+@pytest.mark.parametrize("d", [128, 64])
+def test_segment_mass_key_split(case, qset, d):
     """Per-segment masses with key splits: a chunk that starts or ends inside a segment
     records a partial log-sum-exp for it, the merge combines the chunks that overlap each
     segment; masses match the oracle and the whole-tile launch and add up to the reference
     mass."""
     sizes, cached, n_tgt = case
     n_ref, n_seg = sum(sizes), len(sizes)
-    print(f"segment masses with key splits sizes {sizes} n_tgt {n_tgt} {qset}", flush=True)
-    assert _seg_workspace_bytes(n_ref, n_tgt, 2, 128, qset, "segments", n_seg) > 0, "the launch should split"
-    _, x = _inputs("bf16", 128, n_ref, n_tgt, 1, 2, seed=31)
+    print(f"segment masses with key splits d{d} sizes {sizes} n_tgt {n_tgt} {qset}", flush=True)
+    assert _seg_workspace_bytes(n_ref, n_tgt, 2, d, qset, "segments", n_seg) > 0, "the launch should split"
+    _, x = _inputs("bf16", d, n_ref, n_tgt, 1, 2, seed=31)
     kr, vr, ends = _seg_oracle_inputs(x, sizes, cached)
     got = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached, seg_mass=True)
     whole = _gpu(x, "bf16", qset, "segments", seg_end=ends, seg_cache=cached, seg_mass=True, workspace=False)
