@@ -227,6 +227,12 @@ def cpu_baseline(x, seconds):
     flops = attn_flops(H, total_rows, n_ref + n_tgt, d)
     rate = flops / spent
     full = attn_flops(H, n_ref + n_tgt, n_ref + n_tgt, d)
+    # The oracle's whole launch per workload and mode at the measured rate (its cost is the
+    # same dense products, so it scales with the FLOPs).
+    shapes = {"single_ref": (24, 4352, 4096), "multi_ref": (24, 12544, 4096), "video": (24, 16384, 16384)}
+    whole = {name: {"reuse": round(attn_flops(h, ny, nr + ny, d) / rate, 1),
+                    "full_fresh": round(attn_flops(h, nr + ny, nr + ny, d) / rate, 1)}
+             for name, (h, nr, ny) in shapes.items()}
     return {
         "value": round(rate / 1e12, 6),
         "unit": "TFLOP/s",
@@ -236,6 +242,7 @@ def cpu_baseline(x, seconds):
         f"{n_ref + n_tgt} keys (fp64 numpy oracle, {spent:.1f} s); the whole full-fresh launch would take "
         f"{full / rate:.0f} s at this rate",
         "host": info,
+        "whole_launch_s_at_this_rate": whole,
     }
 
 
