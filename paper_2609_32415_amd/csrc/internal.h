@@ -151,7 +151,7 @@ hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t
 // sends to one XCD (round-robin over the 8 XCDs by launch index) get one
 // contiguous range of tiles; consecutive tiles share (batch, head), so their
 // K/V tiles are re-read from that XCD's L2. A bijection on [0, total).
-__device__ __forceinline__ int xcd_remap(int w, int total) {
+__host__ __device__ __forceinline__ int xcd_remap(int w, int total) {
   const int per = total >> 3, rem = total & 7;
   const int xcd = w & 7, k = w >> 3;
   return xcd * per + (xcd < rem ? xcd : rem) + k;
