@@ -333,6 +333,84 @@ def test_ragged_tiles_never_read_past_the_last_row(d, mode):
         assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
 
 
+# Largest K/V row stride (elements) the bf16 attention accepts: the byte offsets of a 64-row
+# key tile stay below 2^31 (the library rejects larger strides with RA_EUNSUPPORTED).
+MAX_KV_ROW_STRIDE = (1 << 24) - 8
+
+
+def _sparse_rows(a, stride):
+    """A device view of ``a`` ([1, H, S, d], bf16) whose rows lie ``stride`` elements apart in a
+    NaN-filled buffer: any element read outside a row poisons the result."""
+    _, H, S, d = a.shape
+    buf = torch.full((1, H, S, stride), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+    view = buf[..., :d]
+    view.copy_(dev(a, "bf16"))
+    return view
+
+
+# d, n_ref, heads, key-split: two heads whose second starts more than 4 GiB into each buffer, run
+# whole; one head with 10 + 2 key tiles, cut into key chunks by the workspace plan.
+STRIDE_CASES = [(128, 130, 2, False), (64, 130, 2, False), (128, 578, 1, True)]
+
+
+@pytest.mark.parametrize("case", STRIDE_CASES, ids=lambda c: f"d{c[0]}-nref{c[1]}-H{c[2]}-{'split' if c[3] else 'whole'}")
+@pytest.mark.parametrize("mode", [("all", "fresh"), ("target", "cache")], ids=lambda m: "/".join(m))
+def test_largest_kv_row_stride(case, mode):
+    """Every K/V view at the largest accepted row stride (a 64-row key tile spans 2 GiB), with
+    ragged reference and target tails: the 32-bit tile offsets and the 64-bit head, tile and
+    key-chunk bases address the right rows; any other element read is NaN."""
+    d, n_ref, H, split = case
+    qset, kvsrc = mode
+    n_tgt = 70
+    print(f"largest K/V row stride {MAX_KV_ROW_STRIDE} bf16 d {d} n_ref {n_ref} H {H} {qset}/{kvsrc}", flush=True)
+    if split:
+        assert _workspace_bytes(n_ref, n_tgt, H, d, qset, kvsrc) > 0, "the launch should split key ranges"
+    _, x = _inputs("bf16", d, n_ref, n_tgt, B=1, H=H)
+    ref = _oracle(x, qset, kvsrc == "cache")
+    kv = ["k_tgt", "v_tgt"] + (["k_ref_cache", "v_ref_cache"] if kvsrc == "cache" else ["k_ref", "v_ref"])
+    t = {k: (_sparse_rows(v, MAX_KV_ROW_STRIDE) if k in kv else dev(v, "bf16")) for k, v in x.items()}
+    assert t[kv[0]].stride(2) == MAX_KV_ROW_STRIDE
+    if H > 1:
+        assert t[kv[2]].stride(1) * 2 > 1 << 32
+    got = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"],
+                         k_ref=t["k_ref"] if kvsrc == "fresh" else None,
+                         v_ref=t["v_ref"] if kvsrc == "fresh" else None,
+                         k_cache=t["k_ref_cache"] if kvsrc == "cache" else None,
+                         v_cache=t["v_ref_cache"] if kvsrc == "cache" else None,
+                         qset=qset, kvsrc=kvsrc, n_ref=n_ref, lse=True, workspace=None if split else False)
+    torch.cuda.synchronize()
+    del t
+    torch.cuda.empty_cache()
+    assert np.isfinite(host(got.o_tgt)).all() and np.isfinite(host(got.lse)).all()
+    assert max_abs(host(got.o_tgt), ref["tgt"]["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["tgt"]["ref_mass"]) <= MASS_TOL["bf16"]
+    if qset == "all":
+        assert max_abs(host(got.o_ref), ref["ref"]["o"]) <= O_TOL["bf16"]
+
+
+def test_largest_kv_row_stride_segments():
+    """Reference segments alternating between fresh and cached K/V, every K/V view at the
+    largest accepted row stride and the second head more than 4 GiB into each buffer: a load
+    cursor that moves between the two sources keeps its row (only the base pointer changes)."""
+    d, sizes, n_tgt, H, cached = 128, (64, 64, 2), 70, 2, (True, False, True)
+    print(f"largest K/V row stride {MAX_KV_ROW_STRIDE} segments {sizes} cached {cached}", flush=True)
+    _, x = _inputs("bf16", d, sum(sizes), n_tgt, 1, H)
+    kr, vr, ends = _seg_oracle_inputs(x, sizes, cached)
+    big = ("k_tgt", "v_tgt", "k_ref", "v_ref", "k_ref_cache", "v_ref_cache")
+    t = {k: (_sparse_rows(v, MAX_KV_ROW_STRIDE) if k in big else dev(v, "bf16")) for k, v in x.items()}
+    got = ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], k_ref=t["k_ref"], v_ref=t["v_ref"],
+                         k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], qset="target", kvsrc="segments",
+                         n_ref=sum(sizes), seg_end=ends, seg_cache=cached, seg_mass=True, workspace=False)
+    torch.cuda.synchronize()
+    del t
+    torch.cuda.empty_cache()
+    ref = joint_attention(x["q_tgt"], kr, vr, x["k_tgt"], x["v_tgt"])
+    assert np.isfinite(host(got.o_tgt)).all()
+    assert max_abs(host(got.o_tgt), ref["o"]) <= O_TOL["bf16"]
+    assert max_abs(host(got.ref_mass), ref["ref_mass"]) <= MASS_TOL["bf16"]
+    assert max_abs(host(got.seg_mass), segment_masses(x["q_tgt"], kr, x["k_tgt"], ends)) <= MASS_TOL["bf16"]
+
+
 @pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 64)])
 @pytest.mark.parametrize("kvsrc,decision", [("cache", None), ("device", 1), ("device", 2), ("fresh", None)],
                          ids=["cache", "device-REACTIVATE", "device-COMPUTE", "fresh"])
