@@ -586,6 +586,7 @@ SEG_CASES = [
     (128, (300,), 100, 2, (True,)),
     (128, (64,) * 8 + (40,), 128, 2, (True, False) * 4 + (True,)),
     (128, (256, 256), 333, 2, (False, False)),
+    (128, (64,) * 15 + (30,), 100, 2, (True, False, False) * 5 + (True,)),  # RA_MAX_SEG segments
 ]
 
 
@@ -676,6 +677,7 @@ SEG_SPLIT = [
     ((256, 384, 360), (True, False, True), 100),
     ((128,) * 8 + (40,), (True, False) * 4 + (True,), 100),
     ((1000,), (False,), 1100),
+    ((64,) * 15 + (30,), (False, True) * 8, 100),  # RA_MAX_SEG segments, mostly one key tile each
 ]
 
 
