@@ -729,31 +729,40 @@ def test_segment_mass_with_plain_workspace_runs_whole():
     assert torch.equal(got.o_tgt, whole.o_tgt) and torch.equal(got.seg_mass, whole.seg_mass)
 
 
-def _random_cases(n=40, seed=2024):
+def _random_cases(n=40, seed=2024, large=False, first=0):
     """Seeded random configurations: head dim, ragged reference/target sizes (including
     single rows and multiples of the 64-row tile), heads, batch, query set, K/V source,
-    segments (with random tile-aligned boundaries and cache flags) and key splits."""
+    segments (with random tile-aligned boundaries and cache flags) and key splits. ``large``:
+    up to 4000 reference and 2500 target rows, 8 heads and 16 segments."""
     rng = np.random.default_rng(seed)
     cases = []
-    for i in range(n):
+    for i in range(first, first + n):
         d = int(rng.choice([64, 128]))
-        n_ref = int(rng.choice([0, 1, 63, 64, 65, int(rng.integers(2, 700))]))
-        n_tgt = int(rng.choice([1, 64, int(rng.integers(2, 500))]))
-        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+        if large:
+            n_ref = int(rng.choice([0, 64 * int(rng.integers(1, 60)), int(rng.integers(1, 4000))]))
+            n_tgt = int(rng.choice([64 * int(rng.integers(1, 40)), int(rng.integers(1, 2500))]))
+            B, H = int(rng.integers(1, 3)), int(rng.integers(1, 9))
+        else:
+            n_ref = int(rng.choice([0, 1, 63, 64, 65, int(rng.integers(2, 700))]))
+            n_tgt = int(rng.choice([1, 64, int(rng.integers(2, 500))]))
+            B, H = int(rng.integers(1, 3)), int(rng.integers(1, 4))
         qset = str(rng.choice(["target", "all"]))
         kv = str(rng.choice(["fresh", "cache", "segments"])) if n_ref > 0 else "fresh"
         segs, cached = None, None
         if kv == "segments" or (n_ref > 64 and rng.random() < 0.3):
-            cuts = sorted(set(int(x) * 64 for x in rng.integers(1, max(2, (n_ref + 63) // 64), size=3)
+            k = int(rng.integers(1, 16)) if large else 3
+            cuts = sorted(set(int(x) * 64 for x in rng.integers(1, max(2, (n_ref + 63) // 64), size=k)
                               if int(x) * 64 < n_ref))
             segs = cuts + [n_ref]
             cached = [bool(x) for x in rng.integers(0, 2, size=len(segs))]
-        split = bool(rng.random() < 0.5)
+        split = bool(rng.random() < (0.6 if large else 0.5))
         cases.append((i, d, n_ref, n_tgt, B, H, qset, kv, segs, cached, split))
     return cases
 
 
-@pytest.mark.parametrize("case", _random_cases(), ids=lambda c: f"r{c[0]}")
+@pytest.mark.parametrize("case", _random_cases() + [pytest.param(c, marks=pytest.mark.slow)
+                                                     for c in _random_cases(30, 4242, large=True, first=1000)],
+                         ids=lambda c: f"r{c[0]}")
 def test_random_configurations_parity(case):
     i, d, n_ref, n_tgt, B, H, qset, kv, segs, cached, split = case
     print(f"random case {case}", flush=True)
