@@ -43,6 +43,55 @@ def test_q_change_parity(dtype, B, H, n, d, sigma):
     np.testing.assert_allclose(host(got), ref, rtol=1e-5, atol=0)
 
 
+def _layout(t, kind):
+    """``t`` ([B, H, S, d]) as a head-interleaved view ([B, S, H, d] storage) or with its rows
+    padded by 16 NaN elements; "plain" leaves it contiguous."""
+    B, H, S, d = t.shape
+    if kind == "bshd":
+        return t.transpose(1, 2).contiguous().transpose(1, 2)
+    if kind == "pad":
+        buf = torch.full((B, H, S, d + 16), float("nan"), dtype=t.dtype, device=t.device)
+        buf[..., :d] = t
+        return buf[..., :d]
+    return t
+
+
+def _strided_cases(n=16, seed=99):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        cases.append((i, str(rng.choice(["bf16", "f32"])), int(rng.integers(1, 3)), int(rng.integers(1, 33)),
+                      int(rng.choice([1, 63, 65, int(rng.integers(2, 3000)), int(rng.integers(3000, 12000))])),
+                      int(rng.choice([64, 128])), ["plain", "bshd", "pad"][i % 3]))
+    return cases
+
+
+@pytest.mark.parametrize("case", _strided_cases(), ids=lambda c: f"s{c[0]}-{c[1]}-{c[6]}")
+def test_q_change_and_fused_gate_on_strided_views(case):
+    """Q-change and the fused Q-change + gate on contiguous, head-interleaved and padded-row
+    views (NaN in the padding): D matches the oracle and is identical between the two entry
+    points; the fused gate's scores and decision follow the oracle gate."""
+    i, dtype, B, H, n, d, kind = case
+    print(f"q_change strided {case}", flush=True)
+    rng = np.random.default_rng(500 + i)
+    q0 = synth.round_to_dtype(rng.standard_normal((B, H, n, d)).astype(np.float32), dtype)
+    sig = rng.uniform(1e-3, 0.8, (1, H, 1, 1)).astype(np.float32)
+    q1 = synth.round_to_dtype(q0 + sig * rng.standard_normal(q0.shape).astype(np.float32), dtype)
+    m = rng.uniform(0.0, 1.0, (B, H, n)).astype(np.float32)
+    a, b = _layout(dev(q1, dtype), kind), _layout(dev(q0, dtype), kind)
+    got = ops.q_change(a, b)
+    theta = torch.tensor([0.15], dtype=torch.float32, device="cuda:0")
+    d2, dec, score = ops.q_change_gate(a, b, dev(m, "f32"), theta, ops.new_gate_state("cuda:0"), 0, 1, "product")
+    torch.cuda.synchronize()
+    ref = q_change(q1, q0, 1e-8)
+    np.testing.assert_allclose(host(got), ref, rtol=1e-5, atol=0)
+    assert torch.equal(got, d2)
+    exp = gate(ref, m, 0.15, False)
+    np.testing.assert_allclose(host(score), [exp.d_mean, exp.m_mean, exp.g_mean], rtol=1e-5, atol=1e-7)
+    assert abs(exp.g_mean - 0.15) > 1e-4, "the case must not sit on the threshold"
+    assert int(dec.item()) == exp.decision
+
+
 def test_q_change_closed_forms_on_device():
     q = np.random.default_rng(0).standard_normal((1, 3, 100, 64)).astype(np.float32)
     z = ops.q_change(dev(q, "f32"), dev(q, "f32"))
