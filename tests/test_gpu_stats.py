@@ -303,3 +303,24 @@ def test_cache_commit(decision, copied):
         assert torch.equal(ck, src_k) and torch.equal(cv, src_v) and int(age.item()) == 5
     else:
         assert torch.count_nonzero(ck) == 0 and torch.count_nonzero(cv) == 0 and int(age.item()) == -1
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("bf16", 64), ("f32", 64)])
+def test_cache_commit_between_strided_views(dtype, d):
+    """Head-interleaved sources into caches with padded rows (and the reverse for V): every row
+    is copied, and the padding of the destination keeps its sentinel (nothing is written
+    outside the view)."""
+    rng = np.random.default_rng(11)
+    B, H, n = 2, 3, 157
+    src_k = _layout(dev(rng.standard_normal((B, H, n, d)).astype(np.float32), dtype), "bshd")
+    src_v = _layout(dev(rng.standard_normal((B, H, n, d)).astype(np.float32), dtype), "pad")
+    tdt = src_k.dtype
+    buf_k = torch.full((B, H, n, d + 16), 7.0, dtype=tdt, device="cuda:0")
+    dst_k = buf_k[..., :d]
+    dst_k.zero_()
+    dst_v = torch.zeros((B, n, H, d), dtype=tdt, device="cuda:0").transpose(1, 2)
+    dec = torch.tensor([2], dtype=torch.int32, device="cuda:0")
+    ops.cache_commit(src_k, src_v, dst_k, dst_v, decision=dec)
+    torch.cuda.synchronize()
+    assert torch.equal(dst_k, src_k) and torch.equal(dst_v, src_v)
+    assert bool((buf_k[..., d:] == 7.0).all())
