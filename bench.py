@@ -69,6 +69,8 @@ def parse_args():
     ap.add_argument("--no-adaptive", action="store_true",
                     help="skip the depth-adaptive controller trajectory (e.g. for short counter passes)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target duration of the oracle sample")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the register-only MFMA rate probes (mfma_ceiling)")
     ap.add_argument("--sweep", action="store_true", help="also run the 60-block x 8-step controller sweep")
     ap.add_argument("--diagnostics", action="store_true",
                     help="also run the diagnostics sidecar over a 60-block x 8-step controller trajectory")
@@ -244,6 +246,44 @@ def cpu_baseline(x, seconds):
         "host": info,
         "whole_launch_s_at_this_rate": whole,
     }
+
+
+def mfma_ceiling(dev, n_cu, steps=32768, reps=3):
+    """The bf16 MFMA rates of the register-only probes (refadapt_mfma_rate_probe): back-to-back
+    MFMAs, and the attention's per-tile register mix (16 score MFMAs, 16 output MFMAs, 16
+    probability pairs and the rounded-sum dot2s) with no LDS, loads or barrier; one workgroup
+    of 8 wavefronts per CU, operands standard-normal bf16. Each rate is the mean of ``reps``
+    launches of ``steps`` steps (about 50 ms each) after one untimed launch; the shader clock
+    comes from the kernel's own probe."""
+    import torch
+
+    from paper_2609_32415_amd import ops
+
+    gen = torch.Generator().manual_seed(0)
+    operands = torch.randn(32768, generator=gen).to(torch.bfloat16).to(dev)
+    sink = torch.empty(n_cu * 512, dtype=torch.float32, device=dev)
+    flop = float(n_cu) * 8 * steps * 32 * 32768
+    res = {"steps": steps, "workgroups": n_cu}
+    for kind in ("dense", "mix"):
+        ops.mfma_rate_probe(kind, operands, steps, n_cu, sink)
+        probe = torch.zeros(2, dtype=torch.int64, device=dev)
+        ms = []
+        for r in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            ops.mfma_rate_probe(kind, operands, steps, n_cu, sink, clock_probe=probe)
+            e1.record()
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        if not bool(torch.isfinite(sink).all()):
+            raise RuntimeError(f"mfma rate probe {kind}: non-finite sink")
+        cyc, ticks = probe.cpu().tolist()
+        mhz = 100.0 * cyc / ticks if ticks else None
+        tflops = flop / (sum(ms) / len(ms) * 1e-3) / 1e12
+        res[kind] = {"ms": round(sum(ms) / len(ms), 3), "tflops": round(tflops, 1),
+                     "pct_peak": round(100 * tflops / BF16_PEAK_TFLOPS, 2),
+                     "sclk_mhz": round(mhz, 1) if mhz else None}
+    return res
 
 
 def _stats(v):
@@ -489,6 +529,12 @@ def main():
             "traffic": _traffic_from_profile(),
         },
     }
+    if not args.no_ceiling:
+        c = mfma_ceiling(dev, n_cu)
+        c["full_fresh_over_mix"] = round(full_tflops / c["mix"]["tflops"], 4)
+        c["full_fresh_over_dense"] = round(full_tflops / c["dense"]["tflops"], 4)
+        out["mfma_ceiling"] = c
+        log(f"mfma ceiling: {c}")
     del ctl, set0
     torch.cuda.empty_cache()
 

@@ -426,6 +426,30 @@ ra_status refadapt_mass_mean(int32_t batch, int32_t heads, int32_t n_rows, const
 ra_status refadapt_adjacent_mass_change(int32_t n_steps, int32_t n_blocks, int32_t bh, const float* mass_mean,
                                         float* out, void* stream);
 
+/* ---- measurement probe (not part of the method) ----
+ *
+ * refadapt_mfma_rate_probe: the bf16 matrix-core rate this device sustains with every
+ * operand in registers (no LDS, no global loads, no barrier), an upper bound on the joint
+ * attention's rate at the clock the device holds under that load. kind 0
+ * (RA_PROBE_DENSE): 32 back-to-back 32x32x16 bf16 MFMAs per step; kind 1 (RA_PROBE_MIX):
+ * per step the attention's register work of one 64-key tile, 16 score MFMAs and 16
+ * output MFMAs with 16 pairs of probabilities (scale, exp2, row-sum add, bf16 pack) formed
+ * under them. `workgroups` workgroups of 512 threads (one per CU fills the device) each
+ * run `steps` steps: workgroups x 8 x steps x 32 MFMAs of 32768 FLOP.
+ *   operands     device, >= RA_PROBE_OPERAND_BYTES bytes of bf16 values, read once (their
+ *                bit patterns set the matrix core's switching power: pass data like the
+ *                attention's, e.g. standard normal)
+ *   sink         device fp32 [workgroups * 512], written (keeps the work observable)
+ *   clock_probe  device uint64[2] or NULL: thread 0 of each workgroup adds its shader
+ *                cycles and 100 MHz reference ticks (as ra_attn_args.clock_probe)
+ * Errors: RA_EINVAL (kind not 0 or 1, workgroups or steps < 1, null operands or sink),
+ *         RA_EUNSUPPORTED (operands not 16-byte aligned).
+ */
+#define RA_PROBE_OPERAND_BYTES 65536
+enum { RA_PROBE_DENSE = 0, RA_PROBE_MIX = 1 };
+ra_status refadapt_mfma_rate_probe(int32_t kind, int32_t workgroups, int32_t steps, const void* operands,
+                                   float* sink, uint64_t* clock_probe, void* stream);
+
 /* Message describing the calling thread's last non-OK status ("" if none). */
 const char* refadapt_last_error(void);
 

@@ -32,6 +32,9 @@ RA_MAX_SEG = 16
 RA_REUSE, RA_REACTIVATE, RA_COMPUTE = 0, 1, 2
 # ra_gate_mode
 RA_GATE_PRODUCT, RA_GATE_Q_ONLY, RA_GATE_MASS_ONLY, RA_GATE_AND = 0, 1, 2, 3
+# matrix-core rate probe
+RA_PROBE_DENSE, RA_PROBE_MIX = 0, 1
+RA_PROBE_OPERAND_BYTES = 65536
 
 EXPORTED = (
     "refadapt_joint_attn",
@@ -52,6 +55,7 @@ EXPORTED = (
     "refadapt_output_impact",
     "refadapt_mass_mean",
     "refadapt_adjacent_mass_change",
+    "refadapt_mfma_rate_probe",
     "refadapt_last_error",
     "refadapt_version",
 )
@@ -172,6 +176,8 @@ def _load():
     lib.refadapt_mass_mean.restype = i32
     lib.refadapt_adjacent_mass_change.argtypes = [i32, i32, i32, vp, vp, vp]
     lib.refadapt_adjacent_mass_change.restype = i32
+    lib.refadapt_mfma_rate_probe.argtypes = [i32, i32, i32, vp, vp, vp, vp]
+    lib.refadapt_mfma_rate_probe.restype = i32
     lib.refadapt_last_error.argtypes = []
     lib.refadapt_last_error.restype = ctypes.c_char_p
     lib.refadapt_version.argtypes = []
@@ -274,6 +280,10 @@ def refadapt_mass_mean(batch, heads, n_rows, mass, complement, out, stream):
 
 def refadapt_adjacent_mass_change(n_steps, n_blocks, bh, mass_mean, out, stream):
     return _check(LIB.refadapt_adjacent_mass_change(n_steps, n_blocks, bh, mass_mean, out, stream))
+
+
+def refadapt_mfma_rate_probe(kind, workgroups, steps, operands, sink, clock_probe, stream):
+    return _check(LIB.refadapt_mfma_rate_probe(kind, workgroups, steps, operands, sink, clock_probe, stream))
 
 
 def refadapt_last_error():

@@ -666,4 +666,18 @@ ra_status refadapt_adjacent_mass_change(int32_t n_steps, int32_t n_blocks, int32
   return launch_status(e, "adjacent_mass_change");
 }
 
+ra_status refadapt_mfma_rate_probe(int32_t kind, int32_t workgroups, int32_t steps, const void* operands,
+                                   float* sink, uint64_t* clock_probe, void* stream) {
+  static_assert(kProbeOperandBytes == RA_PROBE_OPERAND_BYTES, "probe operand size");
+  if (kind != RA_PROBE_DENSE && kind != RA_PROBE_MIX) return fail(RA_EINVAL, "mfma_rate_probe: unknown kind %d", kind);
+  if (workgroups < 1 || steps < 1) return fail(RA_EINVAL, "mfma_rate_probe: workgroups and steps must be >= 1");
+  if (operands == nullptr || sink == nullptr) return fail(RA_EINVAL, "mfma_rate_probe: null pointer argument");
+  if ((reinterpret_cast<uintptr_t>(operands) & 15) != 0)
+    return fail(RA_EUNSUPPORTED, "mfma_rate_probe: operands must be 16-byte aligned");
+  const hipError_t e = launch_mfma_rate(kind, workgroups, steps, operands, sink,
+                                        reinterpret_cast<unsigned long long*>(clock_probe),
+                                        static_cast<hipStream_t>(stream));
+  return launch_status(e, "mfma_rate_probe");
+}
+
 }  // extern "C"

@@ -16,7 +16,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
-SOURCES = ["api.hip", "attn_bf16.hip", "attn_f32.hip", "stats.hip", "diag.hip"]
+SOURCES = ["api.hip", "attn_bf16.hip", "attn_f32.hip", "stats.hip", "diag.hip", "probe.hip"]
 LIB_NAME = "librefadapt.so"
 ARCH = "gfx950"
 

@@ -127,6 +127,11 @@ hipError_t launch_pair_change(int dtype, int32_t B, int32_t H, int32_t head_dim,
 hipError_t launch_mass_mean(int32_t B, int32_t H, int32_t n, const float* mass, int complement, float* out,
                             hipStream_t stream);
 hipError_t launch_adjacent_change(int32_t T, int32_t nb, int32_t bh, const float* m, float* out, hipStream_t stream);
+// Matrix-core rate probe (measurement only): kind 0 back-to-back MFMAs, kind 1 the
+// attention's per-tile register mix; operands >= kProbeOperandBytes of bf16 data.
+constexpr size_t kProbeOperandBytes = 65536;
+hipError_t launch_mfma_rate(int kind, int32_t workgroups, int32_t steps, const void* operands, float* sink,
+                            unsigned long long* clock_probe, hipStream_t stream);
 
 // Launches `kernel` and returns the status of THIS launch (hipLaunchKernel's
 // return value), not a sticky error left by earlier runtime calls. Arguments

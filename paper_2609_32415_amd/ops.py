@@ -499,3 +499,24 @@ def adjacent_mass_change(mass_log, out=None):
     out = _f32_out("out", out, (nb,), mass_log.device)
     L.refadapt_adjacent_mass_change(T, nb, bh, _ptr(mass_log), _ptr(out), _stream())
     return out
+
+
+def mfma_rate_probe(kind, operands, steps, workgroups=None, sink=None, clock_probe=None):
+    """Runs ``refadapt_mfma_rate_probe`` (``kind`` "dense" or "mix") on the current stream and
+    returns the sink. ``operands``: a device tensor of at least ``RA_PROBE_OPERAND_BYTES``
+    bytes of bf16 values; ``workgroups`` defaults to the device's CU count (one per CU);
+    FLOP = workgroups * 8 * steps * 32 * 32768."""
+    _on_gpu("operands", operands)
+    if operands.numel() * operands.element_size() < L.RA_PROBE_OPERAND_BYTES:
+        raise ValueError(f"operands must hold at least {L.RA_PROBE_OPERAND_BYTES} bytes")
+    if workgroups is None:
+        workgroups = torch.cuda.get_device_properties(operands.device).multi_processor_count
+    if sink is None:
+        sink = torch.empty(workgroups * 512, dtype=torch.float32, device=operands.device)
+    _on_gpu("sink", sink)
+    if sink.dtype != torch.float32 or sink.numel() < workgroups * 512:
+        raise ValueError("sink must be a float32 tensor of at least workgroups * 512 elements")
+    probe = None if clock_probe is None else _ptr(clock_probe)
+    L.refadapt_mfma_rate_probe({"dense": L.RA_PROBE_DENSE, "mix": L.RA_PROBE_MIX}[kind], int(workgroups), int(steps),
+                               _ptr(operands), _ptr(sink), probe, _stream())
+    return sink

@@ -238,3 +238,15 @@ def test_q_change_gate_noalloc_validation():
     assert L.refadapt_q_change_gate_workspace_size(1, 2048, 4096, 128) == 1 << 20  # 32 chunks: fits
     assert L.refadapt_q_change_gate_workspace_size(1, 2048, 8192, 128) == 2 << 20
     assert call(H=2048, n=8192) == L.RA_EUNSUPPORTED and "fixed scratch" in L.refadapt_last_error()
+
+
+def test_mfma_rate_probe_validation():
+    p, odd = ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1004)
+    probe = lambda kind=0, wg=256, steps=10, ops=p, sink=p: L.LIB.refadapt_mfma_rate_probe(
+        kind, wg, steps, ops, sink, None, None)
+    assert probe(kind=2) == L.RA_EINVAL and "kind" in L.refadapt_last_error()
+    assert probe(wg=0) == L.RA_EINVAL
+    assert probe(steps=0) == L.RA_EINVAL
+    assert probe(ops=None) == L.RA_EINVAL
+    assert probe(sink=None) == L.RA_EINVAL
+    assert probe(ops=odd) == L.RA_EUNSUPPORTED

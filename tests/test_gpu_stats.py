@@ -324,3 +324,18 @@ def test_cache_commit_between_strided_views(dtype, d):
     torch.cuda.synchronize()
     assert torch.equal(dst_k, src_k) and torch.equal(dst_v, src_v)
     assert bool((buf_k[..., d:] == 7.0).all())
+
+
+def test_mfma_rate_probe_runs_and_is_deterministic():
+    """Both register-only MFMA probes finish, write finite, repeatable sinks and count a
+    plausible shader clock."""
+    ops_ = torch.randn(32768, generator=torch.Generator().manual_seed(0)).to(torch.bfloat16).cuda()
+    for kind in ("dense", "mix"):
+        print(f"mfma rate probe {kind}", flush=True)
+        probe = torch.zeros(2, dtype=torch.int64, device="cuda:0")
+        a = ops.mfma_rate_probe(kind, ops_, 64, workgroups=8, clock_probe=probe).clone()
+        b = ops.mfma_rate_probe(kind, ops_, 64, workgroups=8)
+        torch.cuda.synchronize()
+        assert bool(torch.isfinite(a).all()) and torch.equal(a, b)
+        cyc, ticks = probe.cpu().tolist()
+        assert ticks > 0 and 300.0 < 100.0 * cyc / ticks < 3000.0
