@@ -9,8 +9,8 @@
 //               then 16 MFMAs of a 128 x 32 output tile whose B operands are the bf16
 //               probabilities of the previous score tile; under the MFMAs, 16 pairs of
 //               scores each take two FMAs (scale, max), two exp2, two row-sum adds and one
-//               bf16 pack, one pair per MFMA slot; after them one dot2 per packed pair sums
-//               the rounded probabilities.
+//               bf16 pack, spread over three consecutive MFMA slots as the attention does;
+//               after the last MFMA one dot2 per packed pair sums the rounded probabilities.
 //
 // One workgroup of eight wavefronts per CU (two per SIMD, as the attention runs). Operands
 // are read once from a caller buffer of random bf16 values (their bit patterns, like the
@@ -84,18 +84,35 @@ __global__ __launch_bounds__(PT, 1) void mfma_rate_kernel(const bf16x8* operands
     // One step: the score MFMAs of the next tile into s_next, the output MFMAs of this tile,
     // and the 16 probability pairs of s_cur (scores 2q, 2q + 1 -> P block q / 4, word q % 4).
     auto step = [&](f32x16(&s_cur)[2], f32x16(&s_next)[2]) {
-      auto pair = [&](int q) {
-        const int mb = q >> 3, o2 = (2 * q) & 15;
-        const float e0 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2], c, -m));
-        const float e1 = __builtin_amdgcn_exp2f(fmaf(s_cur[mb][o2 + 1], c, -m));
-        rs = rs + (e0 + e1);
-        keep(rs);
-        bf16x2 pr;
-        pr[0] = (__bf16)e0;
-        pr[1] = (__bf16)e1;
-        uint32_t w = __builtin_bit_cast(uint32_t, pr);
-        keep(w);
-        pw[q >> 2][q & 3] = w;
+      // Pair q (scores 2q, 2q + 1 -> P block q / 4, word q % 4) in three stages over three
+      // consecutive MFMA slots, as the attention schedules them: exponent arguments, then
+      // the exponentials, then the row-sum adds and the bf16 pack.
+      float pa0 = 0.f, pa1 = 0.f, pe0 = 0.f, pe1 = 0.f;
+      auto slot = [&](int k, int first, int end) {  // pairs first .. end - 1
+        if (k - 2 >= first && k - 2 < end) {
+          const int q = k - 2;
+          rs = rs + (pe0 + pe1);
+          keep(rs);
+          bf16x2 pr;
+          pr[0] = (__bf16)pe0;
+          pr[1] = (__bf16)pe1;
+          uint32_t w = __builtin_bit_cast(uint32_t, pr);
+          keep(w);
+          pw[q >> 2][q & 3] = w;
+        }
+        if (k - 1 >= first && k - 1 < end) {
+          pe0 = __builtin_amdgcn_exp2f(pa0);
+          pe1 = __builtin_amdgcn_exp2f(pa1);
+          keep(pe0);
+          keep(pe1);
+        }
+        if (k >= first && k < end) {
+          const int mb = k >> 3, o2 = (2 * k) & 15;
+          pa0 = fmaf(s_cur[mb][o2], c, -m);
+          pa1 = fmaf(s_cur[mb][o2 + 1], c, -m);
+          keep(pa0);
+          keep(pa1);
+        }
       };
       // The operands are opaque to the compiler at every step (as the attention's, read
       // from LDS, are), so no score MFMA is hoisted out of the loop.
@@ -114,7 +131,7 @@ __global__ __launch_bounds__(PT, 1) void mfma_rate_kernel(const bf16x8* operands
         // key block i >> 3 pairs its A registers with the query blocks in another order
         s_next[i >> 3] =
             __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(i + (i >> 3)) & 3], b[i & 7], s_next[i >> 3], 0, 0, 0);
-        if (i < 10) pair(i);
+        if (i < 12) slot(i, 0, 10);  // pairs 0..9
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
@@ -122,7 +139,7 @@ __global__ __launch_bounds__(PT, 1) void mfma_rate_kernel(const bf16x8* operands
         const int blk = i >> 2;
         const u32x4 pv = {pw[blk][0], pw[blk][1], pw[blk][2], pw[blk][3]};
         o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v[i & 3], __builtin_bit_cast(bf16x8, pv), o[i & 3], 0, 0, 0);
-        if (i < 6) pair(10 + i);  // P blocks 2 and 3 are complete before their first MFMA (i = 8)
+        if (i < 8) slot(10 + i, 10, 16);  // pairs 10..15, P blocks 2 and 3 complete before MFMA 8
         __builtin_amdgcn_sched_barrier(0);
       }
       // the sum of the rounded probabilities, one dot2 per packed pair after the last MFMA
