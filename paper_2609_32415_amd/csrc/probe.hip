@@ -4,13 +4,14 @@
 // matrix instructions plus exactly those, so these rates bound it from above at the clock
 // the device holds under such load.
 //
-//   MFMA_DENSE: 32 v_mfma_f32_32x32x16_bf16 per step in two accumulation chains.
-//   MFMA_MIX:   the attention's per-key-tile register work: 16 MFMAs of a 64 x 32 score tile,
-//               then 16 MFMAs of a 128 x 32 output tile whose B operands are the bf16
-//               probabilities of the previous score tile; under the MFMAs, 16 pairs of
-//               scores each take two FMAs (scale, max), two exp2, two row-sum adds and one
-//               bf16 pack, spread over three consecutive MFMA slots as the attention does;
-//               after the last MFMA one dot2 per packed pair sums the rounded probabilities.
+//   RA_PROBE_DENSE: 32 v_mfma_f32_32x32x16_bf16 per step in two accumulation chains.
+//   RA_PROBE_MIX:   the attention's per-key-tile register work: 16 MFMAs of a 64 x 32 score tile,
+//                   then 16 MFMAs of a 128 x 32 output tile whose B operands are the bf16
+//                   probabilities of the previous score tile; under the MFMAs, 16 pairs of
+//                   scores each take two FMAs (scale, max), two exp2, two row-sum adds and
+//                   one bf16 pack, spread over three consecutive MFMA slots as the attention
+//                   does; after the last MFMA one dot2 per packed pair sums the rounded
+//                   probabilities.
 //
 // One workgroup of eight wavefronts per CU (two per SIMD, as the attention runs). Operands
 // are read once from a caller buffer of random bf16 values (their bit patterns, like the
@@ -47,7 +48,7 @@ __global__ __launch_bounds__(PT, 1) void mfma_rate_kernel(const bf16x8* operands
     clk0 = __builtin_amdgcn_s_memtime();
     rt0 = __builtin_amdgcn_s_memrealtime();
   }
-  // 16 operand registers per lane: four A (key) blocks, eight B (query) blocks, four A (value) blocks.
+  // 16 operand blocks of 8 bf16 per lane: four A (key), eight B (query), four A (value).
   bf16x8 a[4], b[8], v[4];
   const bf16x8* src = operands + (size_t)(wave & 3) * 64 * 16 + lane * 16;
 #pragma unroll
