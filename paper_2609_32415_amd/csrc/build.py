@@ -70,7 +70,30 @@ def build(verbose=False, jobs=4):
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}")
     os.replace(tmp, lib)
+    build_example(verbose)
     return lib
+
+
+def build_example(verbose=False):
+    """Compile examples/joint_attn_c.c, a plain-C caller of the library (C99, the HIP runtime
+    API and include/refadapt.h only), next to its source; it finds the library through its
+    run path."""
+    src = os.path.join(PKG, "examples", "joint_attn_c.c")
+    exe = os.path.join(PKG, "examples", "joint_attn_c")
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        raise RuntimeError("no C compiler found for the C example")
+    cmd = [cc, "-std=c99", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROOT, "include"),
+           "-I", os.path.join(rocm, "include"), src, "-L", PKG, "-lrefadapt", "-L", os.path.join(rocm, "lib"),
+           "-lamdhip64", "-lm", "-Wl,-rpath,$ORIGIN/..", "-Wl,-rpath," + os.path.join(rocm, "lib"), "-o", exe + ".tmp"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"C example build failed:\n{r.stdout}")
+    os.replace(exe + ".tmp", exe)
+    return exe
 
 
 def _drain(procs):

@@ -250,3 +250,34 @@ def test_mfma_rate_probe_validation():
     assert probe(ops=None) == L.RA_EINVAL
     assert probe(sink=None) == L.RA_EINVAL
     assert probe(ops=odd) == L.RA_EUNSUPPORTED
+
+
+def test_header_is_plain_c(tmp_path):
+    """include/refadapt.h compiles as strict C99 and a C program links against the library and
+    calls it (version, argument validation) on a host without a GPU."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "abi.c"
+    src.write_text(
+        '#include <stddef.h>\n#include <string.h>\n#include "refadapt.h"\n'
+        "int main(void) {\n"
+        "  ra_attn_desc d = {1, 24, 128, 4352, 0, RA_BF16, 0.0f, RA_Q_TARGET, RA_KV_CACHE};\n"
+        "  ra_attn_args a;\n"
+        "  memset(&a, 0, sizeof a);\n"
+        "  if (refadapt_joint_attn(&d, &a, NULL) != RA_EINVAL) return 1;\n"
+        '  if (strstr(refadapt_last_error(), "n_tgt") == NULL) return 2;\n'
+        "  if (refadapt_joint_attn_workspace_size(&d) != 0) return 3;\n"
+        '  return strstr(refadapt_version(), "gfx950") == NULL ? 4 : 0;\n'
+        "}\n")
+    exe = tmp_path / "abi"
+    pkg = os.path.dirname(L.LIB_PATH)
+    r = subprocess.run([cc, "-std=c99", "-pedantic", "-Wall", "-Wextra", "-Werror", "-I",
+                        os.path.dirname(HEADER), str(src), "-L", pkg, "-lrefadapt", f"-Wl,-rpath,{pkg}", "-o", str(exe)],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, (r.returncode, r.stdout, r.stderr)
