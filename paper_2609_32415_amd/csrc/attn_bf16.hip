@@ -808,11 +808,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
 // summing the reference part against M_R keeps lse_ref finite when the target
 // keys score so far above the reference keys that 2^(M_R - M) underflows.
 template <int D, int MERGE_BATCH>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+__device__ __forceinline__ void merge_rows(const AttnParams& p, const SplitPlan& pl, bool tgt_only) {
   constexpr int TPR = D / 4, RPB = 256 / TPR;
-  bool tgt_only = false;
-  if (p.kvsrc == KV_DEVICE) tgt_only = __builtin_amdgcn_readfirstlane(*p.decision) == DEC_REUSE;
-  const SplitPlan pl = p.plan[tgt_only ? 1 : 0];
   const int qt_ref = tgt_only ? 0 : p.qt_ref;
   const int r = blockIdx.x * RPB + threadIdx.x / TPR, col = 4 * (threadIdx.x % TPR);
   const int st = r / BM, rr = r - st * BM;
@@ -921,6 +918,22 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
     p.seg_mass[((int64_t)bh * p.n_tgt + qrow) * p.n_seg + s] =
         Ls > 0.f ? __builtin_amdgcn_exp2f(Ms + __log2f(Ls) - (M + __log2f(total))) : 0.f;
   }
+}
+
+template <int D, int MERGE_BATCH>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams p) {
+  bool tgt_only = false;
+  if (p.kvsrc == KV_DEVICE) tgt_only = __builtin_amdgcn_readfirstlane(*p.decision) == DEC_REUSE;
+  const SplitPlan pl = p.plan[tgt_only ? 1 : 0];
+  // Under a device-chosen plan the launch takes the wider instance for the plan with more
+  // chunks; a two-chunk plan then runs the two-chunk body (one batch of loads, no guards).
+  if constexpr (MERGE_BATCH > 2) {
+    if (pl.chunks <= 2) {
+      merge_rows<D, 2>(p, pl, tgt_only);
+      return;
+    }
+  }
+  merge_rows<D, MERGE_BATCH>(p, pl, tgt_only);
 }
 
 // Explicit instantiations: without them the host pass leaves the segment instances, which
