@@ -516,8 +516,8 @@ __global__ __launch_bounds__(NT, 1) void attn_bf16_kernel(AttnParams p) {
     // partner gets the higher priority in phase A and the first one in phase B.
     const bool partner = __builtin_amdgcn_readfirstlane(wave) >= 4;
     if (partner) __builtin_amdgcn_s_setprio(1); else __builtin_amdgcn_s_setprio(0);
-    // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), each followed by one pair of
-    // probabilities of S_j (pairs 0..9: P blocks 0, 1 and half of block 2).
+    // ---- phase A: the MFMAs of S_{j+1} (K_{j+1} is in LDS), with the probability pairs 0..9
+    // of S_j (P blocks 0, 1 and half of block 2) formed under them, three slots per pair.
     // At the last iteration the K buffer holds no tile and S_{j+1} is discarded.
     const uint16_t* kb = kb_next;
     auto k_operand = [&](int i) {  // i = KS * mb + kk
