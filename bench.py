@@ -35,7 +35,6 @@ the per-reference exposure table, ``--diagnostics`` the sidecar trajectory.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import math
 import os
@@ -50,7 +49,6 @@ BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 HBM_PEAK_GBS = 8000.0
 WORKLOAD = "multi_ref"
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "attn_bf16_multi_ref_full_pmc.md")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_32415_amd", "csrc", "attn_bf16.hip")
 
 
 def attn_flops(heads, n_q, n_k, d, batch=1):
@@ -105,16 +103,18 @@ def copy_calibration():
 
 def _traffic_from_profile():
     """HBM bytes per launch of the dominant kernel from the committed rocprofv3
-    --pmc summary, or None when absent or taken on a different kernel source."""
+    --pmc summary, or None when absent or taken on a different build of the kernel (its
+    source or the compile flags)."""
     if not os.path.exists(PMC_SUMMARY):
         return None
     text = open(PMC_SUMMARY).read()
-    m_src = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    m_src = re.search(r"kernel_build_sha256:\s*([0-9a-f]{64})", text)
     m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
     if not m_src or not m_b:
         return None
-    cur = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
-    return float(m_b.group(1)) if cur == m_src.group(1) else None
+    from paper_2609_32415_amd.csrc.build import kernel_build_sha256
+
+    return float(m_b.group(1)) if kernel_build_sha256() == m_src.group(1) else None
 
 
 def time_shapes(dev, reps=10):
