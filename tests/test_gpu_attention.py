@@ -812,3 +812,35 @@ def test_clock_probe_counts_and_leaves_outputs_unchanged():
     mhz = 100.0 * cyc / ticks
     print(f"  mean shader clock {mhz:.0f} MHz", flush=True)
     assert 300.0 < mhz < 3000.0
+
+
+def test_concurrent_launches_on_two_streams():
+    """The library keeps no per-call state outside the caller's buffers: two key-split launches
+    with their own workspaces, enqueued on two streams and running concurrently, give bitwise
+    the outputs of the same launches run one after the other."""
+    print("two streams", flush=True)
+    _, xa = _inputs("bf16", 128, 700, 900, 1, 4, seed=61)
+    _, xb = _inputs("bf16", 128, 300, 1300, 1, 4, seed=62)
+    ta = {k: dev(v, "bf16") for k, v in xa.items()}
+    tb = {k: dev(v, "bf16") for k, v in xb.items()}
+
+    def run(t, kvsrc):
+        return ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"],
+                              v_ref=t["v_ref"], k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], qset="all",
+                              kvsrc=kvsrc, lse=True)
+
+    seq_a, seq_b = run(ta, "fresh"), run(tb, "cache")
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    outs = []
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            a = run(ta, "fresh")
+        with torch.cuda.stream(s2):
+            b = run(tb, "cache")
+        outs.append((a, b))
+    torch.cuda.synchronize()
+    for a, b in outs:
+        for x, y in ((a.o_tgt, seq_a.o_tgt), (a.o_ref, seq_a.o_ref), (a.ref_mass, seq_a.ref_mass), (a.lse, seq_a.lse),
+                     (b.o_tgt, seq_b.o_tgt), (b.o_ref, seq_b.o_ref), (b.ref_mass, seq_b.ref_mass), (b.lse, seq_b.lse)):
+            assert torch.equal(x, y)
