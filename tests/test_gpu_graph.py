@@ -77,3 +77,53 @@ def test_graph_replays_equal_eager_trajectory():
         # eager work on the same stream between replays
         torch.cuda.synchronize()
         assert float(torch.stack([o.float().abs().sum() for o in ctl.o_tgt]).sum()) > 0
+
+
+def test_key_split_attention_graph_follows_the_decision_word():
+    """One device-decided attention launch with a key-split workspace (attention kernel and
+    merge) captured once and replayed with the decision word changed eagerly between replays:
+    every replay equals the eager launch for that decision bitwise."""
+    from paper_2609_32415_amd import ops
+
+    print("graph: key-split attention under RA_KV_DEVICE", flush=True)
+    w = synth.workload("single_ref", heads=2, n_ref=1000, n_tgt=100, seed=5, cache_noise=0.01)
+    x = synth.block_inputs(w)
+    x.update({f"{k}_cache": v for k, v in synth.stale_cache(w, x).items()})
+    t = {k: dev(v, "bf16") for k, v in x.items()}
+    ws = ops.attn_workspace(t["q_tgt"], 1000, "target", "device")
+    assert ws is not False, "the launch should split key ranges"
+    dec = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    o_tgt, o_ref = torch.empty_like(t["q_tgt"]), torch.zeros_like(t["q_ref"])
+    mass = torch.empty(t["q_tgt"].shape[:3], dtype=torch.float32, device="cuda:0")
+
+    def launch():
+        return ops.joint_attn(t["q_tgt"], t["k_tgt"], t["v_tgt"], q_ref=t["q_ref"], k_ref=t["k_ref"],
+                              v_ref=t["v_ref"], k_cache=t["k_ref_cache"], v_cache=t["v_ref_cache"], kvsrc="device",
+                              decision=dec, o_tgt=o_tgt, o_ref=o_ref, ref_mass=mass, workspace=ws)
+
+    want = {}
+    for d in (0, 1, 2):
+        dec.fill_(d)
+        o_ref.zero_()
+        launch()
+        torch.cuda.synchronize()
+        want[d] = (o_tgt.clone(), o_ref.clone(), mass.clone())
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        launch()  # warm-up on the capture stream
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            launch()
+    torch.cuda.synchronize()
+    for rep in range(2):
+        for d in (2, 0, 1):
+            dec.fill_(d)
+            o_ref.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(o_tgt, want[d][0]), (rep, d)
+            assert torch.equal(o_ref, want[d][1]), (rep, d)
+            assert torch.equal(mass, want[d][2]), (rep, d)
