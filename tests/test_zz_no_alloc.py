@@ -49,3 +49,40 @@ def test_noalloc_matches_workspace_entry_point_on_consecutive_calls():
         for a, b in zip(out, ref):
             assert torch.equal(a, b), (i, a, b)
         assert torch.isfinite(out[0]).all() and float(out[0].max()) > 0.0
+
+
+def test_noalloc_in_a_graph_matches_workspace_entry_point_on_each_replay():
+    """Captured once in a HIP graph (what the allocation-free entry point is for) and replayed
+    with new inputs and a reset gate state copied in eagerly between replays: every replay
+    equals the workspace entry point on the same inputs bitwise."""
+    B, H, n, d, block, step = 1, 24, 4096, 128, 0, 1
+    print("noalloc under graph capture", flush=True)
+    th = torch.tensor([0.02], dtype=torch.float32, device="cuda:0")
+    q_cur, q_prev, mass = _inputs(B, H, n, d, torch.bfloat16, 300)
+    state = ops.new_gate_state("cuda:0")
+    init = state.clone()
+    outs = (torch.empty((B, H), dtype=torch.float32, device="cuda:0"),
+            torch.empty(1, dtype=torch.int32, device="cuda:0"), torch.empty(3, dtype=torch.float32, device="cuda:0"))
+    call = lambda: ops.q_change_gate_noalloc(q_cur, q_prev, mass, th, state, block, step, "product",
+                                             d_out=outs[0], decision_out=outs[1], score_out=outs[2])
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        call()  # first call on this device looks up the scratch address, outside the capture
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            call()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        qc, qp, m = _inputs(B, H, n, d, torch.bfloat16, 400 + rep)
+        q_cur.copy_(qc)
+        q_prev.copy_(qp)
+        mass.copy_(m)
+        state.copy_(init)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        ref = _run(ops.q_change_gate, qc, qp, m, th, "product", block, step)
+        for a, b in zip((outs[0].cpu(), outs[1].cpu(), outs[2].cpu(), state.cpu()), ref):
+            assert torch.equal(a, b), (rep, a, b)
