@@ -67,7 +67,7 @@ static tensor make(int rows, int fill, float scale) {
   if (!t.host) exit(3);
   if (fill)
     for (size_t i = 0; i < t.n; ++i) t.host[i] = to_bf16(scale * normal());
-  HIP_OK(hipMalloc(&t.dev, t.n * 2 + 16));
+  HIP_OK(hipMalloc(&t.dev, t.n * 2));
   HIP_OK(hipMemcpy(t.dev, t.host, t.n * 2, hipMemcpyHostToDevice));
   t.view.data = t.dev;
   t.view.stride_b = (int64_t)H * rows * D;
